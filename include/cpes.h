@@ -1,0 +1,243 @@
+/*
+ * cpes.h -- C ABI of the CoPES parameter-space hot path for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * CoPES ("Cooperative Coevolution for Resource-Constrained Agentic LLM
+ * Post-Training", arXiv 2608.02391) is an evolution strategy over all
+ * parameters of a model.  One step (Alg. 1) partitions the d parameters into K
+ * disjoint subspaces (Eq. 7), evaluates seed-defined Gaussian perturbations of
+ * one subspace at a time (Eq. 8, scale sigma_k of Eq. 11), standardises the
+ * rewards of all members jointly (Eq. 12) and adds the reward-weighted noise
+ * back to the parameters (Eq. 13; Eq. 6 for standard ES).  Noise is never
+ * stored: every call regenerates it from the member's seed (Sec. 3.3 and
+ * Supp. A.8, "Seed Replay and Chunking"), and the pre-perturbation weights are
+ * restored from a backup rather than by subtraction ("CPU Weight Backup").
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers named *_dev are device pointers (e.g. a torch tensor's data_ptr());
+ * pointers named *_host are host pointers.  The caller owns every buffer; the
+ * library keeps no pointer and no state between calls besides a thread-local
+ * error string.  `stream` is a hipStream_t passed as void* (NULL = the null
+ * stream).  Every call only enqueues work on `stream` and returns without
+ * synchronising; a kernel failure surfaces at the caller's next
+ * synchronisation.  Arguments are validated on the host before anything is
+ * enqueued, so a call that returns an error has had no effect.  No call
+ * allocates device memory; scratch space comes in through `workspace`.
+ * Results depend only on the arguments (not on the stream, launch geometry or
+ * run).
+ *
+ * Weights are a flat buffer of `numel` elements of dtype CPES_BF16 or
+ * CPES_F32.  A subspace (cpes_subspace) lists `length` positions j = 0 ..
+ * length-1; position j is parameter `offset + j` (index == NULL) or parameter
+ * `index[offset + j]` (index = device array of int64 parameter indices, the
+ * embedding P_k of Eq. 8).  Index entries outside [0, numel) are skipped.
+ *
+ * Noise.  Position j of the noise of a member with seed s is
+ *   eps_j = BoxMuller(Philox4x32-10(counter = (lo32 q, hi32 q, 0, 0),
+ *                                   key = (lo32 s, hi32 s)), j mod 4),
+ * q = j / 4: words (x0, x1) give positions 4q and 4q+1, words (x2, x3) give
+ * 4q+2 and 4q+3; radius sqrt(-2 ln U(a)), angle 2 pi U(b), U(x) = ((x >> 8) +
+ * 1) 2^-24; cosine for the even position, sine for the odd one; evaluated in
+ * fp64 and rounded once to fp32.
+ */
+#ifndef CPES_H
+#define CPES_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CPES_ABI_VERSION 1
+
+/* Exported symbols (the library is built with hidden default visibility). */
+#define CPES_API __attribute__((visibility("default")))
+
+/* Status codes returned by every int-valued entry point. */
+enum cpes_status {
+    CPES_OK = 0,
+    CPES_ERR_INVALID_ARGUMENT = -1, /* a null, out-of-range or inconsistent argument */
+    CPES_ERR_UNSUPPORTED = -2,      /* valid but beyond this build's limits (see each call) */
+    CPES_ERR_WORKSPACE = -3,        /* workspace missing or smaller than required */
+    CPES_ERR_HIP = -4,              /* the HIP runtime reported an error while enqueueing */
+};
+
+enum cpes_dtype { CPES_BF16 = 0, CPES_F32 = 1 };
+enum cpes_partition_mode { CPES_PART_CONTIGUOUS = 0, CPES_PART_PERMUTATION = 1 };
+enum cpes_aux_mode { CPES_AUX_NONE = 0, CPES_AUX_SNAPSHOT = 1, CPES_AUX_MASTER = 2 };
+enum cpes_norm_mode { CPES_NORM_Z = 0, CPES_NORM_RANK = 1 };
+enum cpes_scale_mode { CPES_SCALE_ALPHA_OVER_N_SIGMA = 0, CPES_SCALE_ALPHA_OVER_N = 1 };
+
+/* Limits of this build. */
+#define CPES_MAX_MEMBERS 256         /* members per cpes_update call */
+#define CPES_MAX_REWARDS 4096        /* rewards per cpes_normalize_rewards call */
+#define CPES_MAX_GROUPS 1024         /* reward groups per cpes_normalize_rewards call */
+#define CPES_MAX_PERMUTATION_K 256   /* subspaces of a CPES_PART_PERMUTATION partition */
+
+typedef struct cpes_subspace {
+    int64_t offset;        /* first parameter (index == NULL) or first map entry */
+    int64_t length;        /* number of positions d_k, >= 0 */
+    const int64_t* index;  /* NULL, or device int64 map read at [offset, offset + length) */
+} cpes_subspace;
+
+/*
+ * cpes_partition -- subspaces of Eq. (7): disjoint, covering all d indices,
+ * sizes d/K (differing by at most one when K does not divide d).  The paper
+ * resamples the partition every step from a stored seed and replays it
+ * (Sec. 3.3, Supp. A.8 "Partition Replay").
+ *
+ * mode CPES_PART_CONTIGUOUS: offsets_host[k] = bounds_host[k] (K+1 values,
+ *   non-decreasing from 0 to d) or, with bounds_host == NULL, floor(k d / K).
+ *   Subspace k is the parameter range [offsets[k], offsets[k+1]).  Host only:
+ *   nothing is enqueued, index_dev / workspace may be NULL.
+ * mode CPES_PART_PERMUTATION: element i belongs to subspace
+ *   floor(E(i) K / d), where E is a keyed pseudo-random permutation of [0, d):
+ *   an 8-round balanced Feistel network on b = max(2, ceil(log2 d)) (rounded
+ *   up to even) bits whose round r function is word 0 of the Philox block
+ *   (counter (R, r, 3, 0), key seed) masked to b/2 bits, restricted to [0, d)
+ *   by cycle-walking.  index_dev (device int64[d]) receives, for each k, the
+ *   members of subspace k in ascending order at [offsets[k], offsets[k+1]),
+ *   and offsets_host[k] = ceil(k d / K) (exact because E is a bijection).
+ *   Requires 1 <= K <= CPES_MAX_PERMUTATION_K, d < 2^55 and a device workspace of
+ *   cpes_partition_workspace_bytes() bytes (16-byte aligned).
+ * status_dev: NULL, or a device int32 set to 0, or to 1 if a cycle walk
+ *   exceeded its bound (cannot happen for a bijection; a safety net).
+ * Errors: d < 1 or d >= 2^62, K < 1 or K > d, bad bounds, mode unknown,
+ *   index_dev NULL for PERMUTATION -> CPES_ERR_INVALID_ARGUMENT; K above the
+ *   limit -> CPES_ERR_UNSUPPORTED; workspace too small -> CPES_ERR_WORKSPACE.
+ */
+CPES_API int cpes_partition(int mode, int64_t d, int32_t K, uint64_t seed, const int64_t* bounds_host,
+                   int64_t* offsets_host, int64_t* index_dev, void* workspace_dev,
+                   size_t workspace_bytes, int32_t* status_dev, void* stream);
+
+/* Workspace bytes cpes_partition needs (0 for CONTIGUOUS); 0 for invalid arguments. */
+CPES_API size_t cpes_partition_workspace_bytes(int mode, int64_t d, int32_t K);
+
+/*
+ * cpes_perturb -- theta_{k,i} = theta + sigma_k P_k eps_{k,i} (Eq. 8, Alg. 1),
+ * in place on the subspace `s` of w (numel elements of `dtype`):
+ *   w[p(j)] = cast(fmaf(sign * sigma, eps_j(seed), src_j)),  j < s->length,
+ * one fp32 fused multiply-add, then round-to-nearest-even for bf16.
+ * sigma is the effective scale sigma_k = sigma sqrt(d / d_k) (Eq. 11);
+ * sign is +1 or -1 (mirrored pairs).
+ *   aux_mode CPES_AUX_NONE:     src_j = w[p(j)]; aux ignored.
+ *   aux_mode CPES_AUX_SNAPSHOT: src_j = w[p(j)], and aux (device, dtype of w,
+ *                               s->length elements) receives aux[j] = w[p(j)]
+ *                               before the change: the weight backup.
+ *   aux_mode CPES_AUX_MASTER:   src_j = ((const float*)aux)[j], an fp32 master
+ *                               of the subspace (CPES_BF16 weights only).
+ * Parameters outside the subspace are not touched.
+ * Errors: w NULL, s NULL, length < 0, contiguous range beyond numel, dtype /
+ *   aux_mode unknown, aux NULL when needed, sign not +-1, sigma negative or
+ *   not finite, MASTER with fp32 weights -> CPES_ERR_INVALID_ARGUMENT.
+ */
+CPES_API int cpes_perturb(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float sigma,
+                 uint64_t seed, int32_t sign, void* aux_dev, int aux_mode, void* stream);
+
+/*
+ * cpes_restore -- undo a perturbation (Sec. 3.3):
+ *   CPES_AUX_SNAPSHOT: w[p(j)] = aux[j] (bit copy; exact).
+ *   CPES_AUX_MASTER:   w[p(j)] = rne_bf16(((const float*)aux)[j]) (exact when
+ *                      the master was staged from w).
+ *   CPES_AUX_NONE:     replay: w[p(j)] = cast(fmaf(-sign * sigma, eps_j, w[p(j)])).
+ *                      Not an identity in floating point; the paper's reason for
+ *                      keeping a backup.  Differs by at most one fp32 ulp (more
+ *                      after bf16 rounding).
+ * Arguments and errors as cpes_perturb (sigma, seed, sign only used by NONE).
+ */
+CPES_API int cpes_restore(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float sigma,
+                 uint64_t seed, int32_t sign, const void* aux_dev, int aux_mode, void* stream);
+
+/*
+ * cpes_stage_master -- master_dev[j] = fp32 value of w[p(j)] (exact), the fp32
+ * master copy of the active subspace kept while its bf16 weights are
+ * perturbed and updated.  Errors as cpes_perturb.
+ */
+CPES_API int cpes_stage_master(const void* w_dev, int64_t numel, int dtype, const cpes_subspace* s,
+                      float* master_dev, void* stream);
+
+/*
+ * cpes_normalize_rewards -- reward standardisation.
+ *   CPES_NORM_Z:    Eq. (5) / Eq. (12): mu = sum r / n, s = sqrt(sum (r - mu)^2 / n)
+ *                   (population std, sums in fp64 in index order);
+ *                   out = (r - mu) / s, or 0 for every member when s == 0.
+ *   CPES_NORM_RANK: centred average rank a / (n - 1) - 1/2 with a the 0-based
+ *                   rank and ties sharing the mean of their ranks; 0 when n == 1.
+ * group_dev == NULL standardises all n rewards jointly (Eq. 12).  Otherwise
+ * group_dev (device int32[n], values in [0, n_groups)) standardises each group
+ * on its own (independent standardisation, the ablation of Sec. 4.4).
+ * r_dev and out_dev are device float32[n] and may alias.  status_dev (NULL or
+ * device int32) receives 0, 1 if a reward is not finite, or 2 if a group id is
+ * out of range; in both failure cases every output is 0 (so an update leaves
+ * the weights unchanged).
+ * Errors: NULL r_dev / out_dev, n outside [1, CPES_MAX_REWARDS], unknown mode,
+ *   n_groups outside [1, n] with group_dev given -> CPES_ERR_INVALID_ARGUMENT;
+ *   n_groups above CPES_MAX_GROUPS -> CPES_ERR_UNSUPPORTED.
+ */
+CPES_API int cpes_normalize_rewards(const float* r_dev, int32_t n, int mode, const int32_t* group_dev,
+                           int32_t n_groups, float* out_dev, int32_t* status_dev, void* stream);
+
+/*
+ * cpes_update -- seed-replayed ES update of one subspace (Eq. 6 / Eq. 13;
+ * Sec. 3.3):  theta_S += step * sum_i sign_i * rnorm_i * eps(seed_i),
+ *   step = alpha / (n * sigma)   (CPES_SCALE_ALPHA_OVER_N_SIGMA, OpenAI-ES form)
+ *   step = alpha / n             (CPES_SCALE_ALPHA_OVER_N, the paper's form with
+ *                                 n = N_k members of this subspace).
+ * seeds_host / signs_host (host, n entries; signs +-1) describe the members in
+ * the order their rewards appear in rnorm_dev (device float32[n], typically
+ * the output of cpes_normalize_rewards).  Members sharing a seed (mirrored
+ * pairs) share one noise vector, which is generated once with coefficient
+ * sum(sign * rnorm).  Each weight is read once and written once; the weighted
+ * noise sum is accumulated in fp32 in order of first appearance of each seed.
+ *   master_dev == NULL: w[p(j)] = cast(fmaf(step, acc_j, w[p(j)])).
+ *   master_dev != NULL: master[j] = fmaf(step, acc_j, master[j]) and
+ *                       w[p(j)] = cast(master[j]) (device float32[length]).
+ * Errors: NULL pointers, n outside [1, CPES_MAX_MEMBERS] (UNSUPPORTED above),
+ *   a sign not +-1, alpha or sigma not finite, sigma <= 0 with the
+ *   OVER_N_SIGMA scale, dtype / scale_mode unknown, contiguous range beyond
+ *   numel -> CPES_ERR_INVALID_ARGUMENT.
+ */
+CPES_API int cpes_update(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float* master_dev,
+                int32_t n, const uint64_t* seeds_host, const int8_t* signs_host,
+                const float* rnorm_dev, float alpha, float sigma, int scale_mode, void* stream);
+
+/* ---------------- test hooks and measurement utilities ------------------ */
+
+/* out_dev[4 b + t] = word t of the Philox block q0 + b of stream (seed, domain),
+ * b < nblocks.  Errors: out_dev NULL, nblocks < 0. */
+CPES_API int cpes_debug_philox(uint64_t seed, uint32_t domain, uint64_t q0, int64_t nblocks,
+                      uint32_t* out_dev, void* stream);
+
+/* out_dev[k] = eps_{j0 + k}(seed) for k < n (the noise perturb/update use). */
+CPES_API int cpes_debug_normals(uint64_t seed, int64_t j0, int64_t n, float* out_dev, void* stream);
+
+/* The two halves of the normal transform on the grid m = m0 + k, k < n,
+ * 1 <= m <= 2^24 (word (m - 1) << 8): rho_dev[k] = sqrt(-2 ln(m 2^-24)),
+ * (cos_dev[k], sin_dev[k]) = (cos, sin)(pi m 2^-23), all fp64 (any may be NULL). */
+CPES_API int cpes_debug_bm_grid(uint32_t m0, int64_t n, double* rho_dev, double* cos_dev,
+                       double* sin_dev, void* stream);
+
+/* The partition permutation of cpes_partition on i = i0 + k, k < n:
+ * perm_dev[k] = E(i) (may be NULL), bucket_dev[k] = floor(E(i) K / d) (may be NULL). */
+CPES_API int cpes_debug_prp(uint64_t seed, int64_t d, int32_t K, int64_t i0, int64_t n,
+                   int64_t* perm_dev, int32_t* bucket_dev, void* stream);
+
+/* RNG-only throughput probe: generates n normals of stream `seed` (positions
+ * 0 .. n-1) and folds them into sink_dev[0] (one uint32, overwritten) without
+ * other memory traffic, to measure the generator's ALU ceiling. */
+CPES_API int cpes_rng_probe(uint64_t seed, int64_t n, uint32_t* sink_dev, void* stream);
+
+/* Message of the last error on the calling thread ("" if none). */
+CPES_API const char* cpes_last_error(void);
+
+/* CPES_ABI_VERSION of the built library. */
+CPES_API int cpes_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CPES_H */

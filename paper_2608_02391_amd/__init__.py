@@ -1,0 +1,213 @@
+"""Python binding of ``libcpes`` -- the gfx950 C-ABI library of the CoPES
+parameter-space hot path (see ``include/cpes.h``).
+
+Argument marshalling only: every step runs in the library's HIP kernels.
+Tensors must live on the GPU; streams default to torch's current stream.
+There is no CPU fallback: if ``libcpes.so`` is missing or fails to load, every
+call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libcpes.so")
+
+OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
+BF16, F32 = 0, 1
+PART_CONTIGUOUS, PART_PERMUTATION = 0, 1
+AUX_NONE, AUX_SNAPSHOT, AUX_MASTER = 0, 1, 2
+NORM_Z, NORM_RANK = 0, 1
+SCALE_ALPHA_OVER_N_SIGMA, SCALE_ALPHA_OVER_N = 0, 1
+MAX_MEMBERS, MAX_REWARDS, MAX_GROUPS, MAX_PERMUTATION_K = 256, 4096, 1024, 256
+
+EXPORTED = (
+    "cpes_partition", "cpes_partition_workspace_bytes", "cpes_perturb", "cpes_restore",
+    "cpes_stage_master", "cpes_normalize_rewards", "cpes_update", "cpes_debug_philox",
+    "cpes_debug_normals", "cpes_debug_bm_grid", "cpes_debug_prp", "cpes_rng_probe",
+    "cpes_last_error", "cpes_abi_version",
+)
+
+
+class CpesError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{message} (status {code})")
+        self.code = code
+
+
+class Subspace(ctypes.Structure):
+    _fields_ = [("offset", ctypes.c_int64), ("length", ctypes.c_int64), ("index", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load ``libcpes.so`` (built by ``paper_2608_02391_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2608_02391_amd.build`")
+    L = ctypes.CDLL(path)
+    vp, i64, u64, i32, u32, f32 = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int32,
+                                   ctypes.c_uint32, ctypes.c_float)
+    sp = ctypes.POINTER(Subspace)
+    sig = {
+        "cpes_partition": [i32, i64, i32, u64, vp, vp, vp, vp, ctypes.c_size_t, vp, vp],
+        "cpes_partition_workspace_bytes": [i32, i64, i32],
+        "cpes_perturb": [vp, i64, i32, sp, f32, u64, i32, vp, i32, vp],
+        "cpes_restore": [vp, i64, i32, sp, f32, u64, i32, vp, i32, vp],
+        "cpes_stage_master": [vp, i64, i32, sp, vp, vp],
+        "cpes_normalize_rewards": [vp, i32, i32, vp, i32, vp, vp, vp],
+        "cpes_update": [vp, i64, i32, sp, vp, i32, vp, vp, vp, f32, f32, i32, vp],
+        "cpes_debug_philox": [u64, u32, u64, i64, vp, vp],
+        "cpes_debug_normals": [u64, i64, i64, vp, vp],
+        "cpes_debug_bm_grid": [u32, i64, vp, vp, vp, vp],
+        "cpes_debug_prp": [u64, i64, i32, i64, i64, vp, vp, vp],
+        "cpes_rng_probe": [u64, i64, vp, vp],
+        "cpes_last_error": [],
+        "cpes_abi_version": [],
+    }
+    for name, args in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    L.cpes_partition_workspace_bytes.restype = ctypes.c_size_t
+    L.cpes_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def last_error() -> str:
+    return load().cpes_last_error().decode()
+
+
+def _check(rc: int) -> None:
+    if rc != OK:
+        raise CpesError(rc, last_error())
+
+
+# ----------------------------------------------------------- marshalling --
+
+def _torch():
+    import torch
+
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"weights must be bfloat16 or float32, not {t.dtype}")
+
+
+def _dev_ptr(t, what: str) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return _torch().cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def subspace(offset: int, length: int, index=None) -> Subspace:
+    """Positions j < length at parameter offset + j, or index[offset + j]."""
+    if index is not None and index.dtype != _torch().int64:
+        raise TypeError("index map must be int64")
+    return Subspace(int(offset), int(length), _dev_ptr(index, "index map"))
+
+
+# ------------------------------------------------------------- entry points --
+
+def cpes_partition(mode: int, d: int, K: int, seed: int = 0, bounds: Optional[Sequence[int]] = None,
+                   index=None, workspace=None, status=None, stream=None):
+    """Returns the K+1 subspace offsets (host ints); PERMUTATION fills ``index``."""
+    L = load()
+    offsets = (ctypes.c_int64 * (K + 1))()
+    b = None if bounds is None else (ctypes.c_int64 * (K + 1))(*[int(x) for x in bounds])
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(L.cpes_partition(mode, d, K, seed, b, offsets, _dev_ptr(index, "index"),
+                            _dev_ptr(workspace, "workspace"), ws_bytes, _dev_ptr(status, "status"),
+                            _stream(stream)))
+    return [int(x) for x in offsets]
+
+
+def cpes_partition_workspace_bytes(mode: int, d: int, K: int) -> int:
+    return int(load().cpes_partition_workspace_bytes(mode, d, K))
+
+
+def cpes_perturb(w, s: Subspace, sigma: float, seed: int, sign: int, aux=None, aux_mode: int = AUX_NONE,
+                 stream=None) -> None:
+    _check(load().cpes_perturb(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s), sigma, seed, sign,
+                               _dev_ptr(aux, "aux"), aux_mode, _stream(stream)))
+
+
+def cpes_restore(w, s: Subspace, sigma: float = 0.0, seed: int = 0, sign: int = 1, aux=None,
+                 aux_mode: int = AUX_SNAPSHOT, stream=None) -> None:
+    _check(load().cpes_restore(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s), sigma, seed, sign,
+                               _dev_ptr(aux, "aux"), aux_mode, _stream(stream)))
+
+
+def cpes_stage_master(w, s: Subspace, master, stream=None) -> None:
+    _check(load().cpes_stage_master(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s),
+                                    _dev_ptr(master, "master"), _stream(stream)))
+
+
+def cpes_normalize_rewards(r, out, mode: int = NORM_Z, group=None, n_groups: int = 1, status=None,
+                           stream=None) -> None:
+    _check(load().cpes_normalize_rewards(_dev_ptr(r, "rewards"), r.numel(), mode, _dev_ptr(group, "group"),
+                                         n_groups, _dev_ptr(out, "out"), _dev_ptr(status, "status"),
+                                         _stream(stream)))
+
+
+def cpes_update(w, s: Subspace, seeds: Sequence[int], signs: Sequence[int], rnorm, alpha: float, sigma: float,
+                scale_mode: int = SCALE_ALPHA_OVER_N_SIGMA, master=None, stream=None) -> None:
+    n = len(seeds)
+    if len(signs) != n:
+        raise ValueError("seeds and signs differ in length")
+    cs = (ctypes.c_uint64 * n)(*[int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds])
+    cg = (ctypes.c_int8 * n)(*[int(x) for x in signs])
+    _check(load().cpes_update(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s),
+                              _dev_ptr(master, "master"), n, cs, cg, _dev_ptr(rnorm, "rnorm"), alpha, sigma,
+                              scale_mode, _stream(stream)))
+
+
+def cpes_debug_philox(seed: int, domain: int, q0: int, nblocks: int, out, stream=None) -> None:
+    _check(load().cpes_debug_philox(seed, domain, q0, nblocks, _dev_ptr(out, "out"), _stream(stream)))
+
+
+def cpes_debug_normals(seed: int, j0: int, n: int, out, stream=None) -> None:
+    _check(load().cpes_debug_normals(seed, j0, n, _dev_ptr(out, "out"), _stream(stream)))
+
+
+def cpes_debug_bm_grid(m0: int, n: int, rho=None, cos=None, sin=None, stream=None) -> None:
+    _check(load().cpes_debug_bm_grid(m0, n, _dev_ptr(rho, "rho"), _dev_ptr(cos, "cos"), _dev_ptr(sin, "sin"),
+                                     _stream(stream)))
+
+
+def cpes_debug_prp(seed: int, d: int, K: int, i0: int, n: int, perm=None, bucket=None, stream=None) -> None:
+    _check(load().cpes_debug_prp(seed, d, K, i0, n, _dev_ptr(perm, "perm"), _dev_ptr(bucket, "bucket"),
+                                 _stream(stream)))
+
+
+def cpes_rng_probe(seed: int, n: int, sink, stream=None) -> None:
+    _check(load().cpes_rng_probe(seed, n, _dev_ptr(sink, "sink"), _stream(stream)))
+
+
+def cpes_abi_version() -> int:
+    return int(load().cpes_abi_version())

@@ -1,0 +1,399 @@
+// cpes_api.hip -- host runtime behind include/cpes.h: argument validation,
+// dispatch to the gfx950 kernels, error reporting.  Every check runs before
+// anything is enqueued, so a failing call has no effect; no HIP call is made
+// before validation passes (the library loads and validates without a GPU).
+#include "cpes.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "cpes_launch.hpp"
+
+namespace {
+
+thread_local std::string g_error;
+
+int fail(int code, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return code;
+}
+
+int hip_status(hipError_t e, const char* what)
+{
+    if (e != hipSuccess) return fail(CPES_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return CPES_OK;
+}
+
+bool aligned16(const void* p)
+{
+    return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
+}
+
+size_t elem_size(int dtype)
+{
+    return dtype == CPES_BF16 ? 2 : 4;
+}
+
+// Common checks of a subspace on a weight buffer.
+int check_subspace(const void* w, int64_t numel, int dtype, const cpes_subspace* s, const char* fn)
+{
+    if (!w) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: weight pointer is null", fn);
+    if (dtype != CPES_BF16 && dtype != CPES_F32) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown dtype %d", fn, dtype);
+    if (!s) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: subspace is null", fn);
+    if (numel < 0) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: numel %lld < 0", fn, (long long)numel);
+    if (s->length < 0 || s->offset < 0)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: negative offset %lld or length %lld", fn, (long long)s->offset,
+                    (long long)s->length);
+    if (s->length > (INT64_MAX / 8) - s->offset)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: offset + length overflows", fn);
+    if (!s->index && s->offset + s->length > numel)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: range [%lld, %lld) exceeds numel %lld", fn, (long long)s->offset,
+                    (long long)(s->offset + s->length), (long long)numel);
+    return CPES_OK;
+}
+
+int check_sign(int32_t sign, const char* fn)
+{
+    if (sign != 1 && sign != -1) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: sign %d is not +1 or -1", fn, sign);
+    return CPES_OK;
+}
+
+int check_sigma(float sigma, const char* fn)
+{
+    if (!std::isfinite(sigma) || sigma < 0.0f)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: sigma %g is negative or not finite", fn, (double)sigma);
+    return CPES_OK;
+}
+
+// Whether the 16-byte vector path applies: every unit's vectors are aligned.
+bool vector_ok(const void* w, int dtype, const cpes_subspace* s, const void* aux, bool aux_is_master)
+{
+    if (s->index) {
+        if (!aligned16(s->index + s->offset)) return false;
+    } else {
+        const char* base = static_cast<const char*>(w) + (size_t)s->offset * elem_size(dtype);
+        if (!aligned16(base)) return false;
+    }
+    if (aux && !aligned16(aux)) return false;
+    (void)aux_is_master;
+    return true;
+}
+
+cpes::StreamArgs stream_args(void* w, int64_t numel, const cpes_subspace* s, const void* aux, uint64_t seed,
+                             float scale)
+{
+    cpes::StreamArgs a;
+    a.w = w;
+    a.index = s->index;
+    a.aux = const_cast<void*>(aux);
+    a.offset = s->offset;
+    a.length = s->length;
+    a.numel = numel;
+    a.k0 = (uint32_t)seed;
+    a.k1 = (uint32_t)(seed >> 32);
+    a.scale = scale;
+    return a;
+}
+
+int feistel_half_bits(int64_t d)
+{
+    int b = 0;
+    while (b < 63 && ((int64_t)1 << b) < d) ++b;
+    if (b < 2) b = 2;
+    if (b & 1) ++b;
+    return b / 2;
+}
+
+struct PartitionLayout {
+    int64_t n_tiles, n_counts, scan_blocks;
+    size_t off_counts, off_pos, off_block_sums, total;
+};
+
+size_t round_up(size_t x, size_t a)
+{
+    return (x + a - 1) / a * a;
+}
+
+PartitionLayout partition_layout(int64_t d, int32_t K)
+{
+    PartitionLayout L;
+    L.n_tiles = (d + cpes::kTile - 1) / cpes::kTile;
+    L.n_counts = (int64_t)K * L.n_tiles;
+    L.scan_blocks = (L.n_counts + cpes::kScanChunk - 1) / cpes::kScanChunk;
+    L.off_counts = round_up((size_t)d, 256);
+    L.off_pos = round_up(L.off_counts + (size_t)L.n_counts * 4, 256);
+    L.off_block_sums = round_up(L.off_pos + (size_t)L.n_counts * 8, 256);
+    L.total = round_up(L.off_block_sums + (size_t)L.scan_blocks * 8, 256);
+    return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* cpes_last_error(void)
+{
+    return g_error.c_str();
+}
+
+int cpes_abi_version(void)
+{
+    return CPES_ABI_VERSION;
+}
+
+size_t cpes_partition_workspace_bytes(int mode, int64_t d, int32_t K)
+{
+    if (mode == CPES_PART_CONTIGUOUS) return 0;
+    if (mode != CPES_PART_PERMUTATION || d < 1 || K < 1 || K > CPES_MAX_PERMUTATION_K || (int64_t)K > d ||
+        d >= ((int64_t)1 << 55))
+        return 0;
+    return partition_layout(d, K).total;
+}
+
+int cpes_partition(int mode, int64_t d, int32_t K, uint64_t seed, const int64_t* bounds_host, int64_t* offsets_host,
+                   int64_t* index_dev, void* workspace_dev, size_t workspace_bytes, int32_t* status_dev, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_partition";
+    if (mode != CPES_PART_CONTIGUOUS && mode != CPES_PART_PERMUTATION)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown mode %d", fn, mode);
+    if (d < 1 || d >= ((int64_t)1 << 62)) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: d %lld out of range", fn, (long long)d);
+    if (K < 1 || (int64_t)K > d) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: K %d not in [1, d]", fn, K);
+    if (!offsets_host) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: offsets_host is null", fn);
+    if (mode == CPES_PART_CONTIGUOUS) {
+        if (bounds_host) {
+            if (bounds_host[0] != 0 || bounds_host[K] != d)
+                return fail(CPES_ERR_INVALID_ARGUMENT, "%s: bounds must run from 0 to d", fn);
+            for (int32_t k = 0; k < K; ++k)
+                if (bounds_host[k + 1] < bounds_host[k])
+                    return fail(CPES_ERR_INVALID_ARGUMENT, "%s: bounds decrease at %d", fn, k);
+            for (int32_t k = 0; k <= K; ++k) offsets_host[k] = bounds_host[k];
+        } else {
+            for (int32_t k = 0; k <= K; ++k)
+                offsets_host[k] = (int64_t)(((unsigned __int128)(uint64_t)d * (uint64_t)k) / (uint64_t)K);
+        }
+        return CPES_OK;
+    }
+    if (K > CPES_MAX_PERMUTATION_K)
+        return fail(CPES_ERR_UNSUPPORTED, "%s: K %d above CPES_MAX_PERMUTATION_K", fn, K);
+    if (d >= ((int64_t)1 << 55)) return fail(CPES_ERR_UNSUPPORTED, "%s: permutation needs d < 2^55", fn);
+    if (!index_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: index_dev is null", fn);
+    const PartitionLayout L = partition_layout(d, K);
+    if (!workspace_dev || workspace_bytes < L.total)
+        return fail(CPES_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, L.total,
+                    workspace_dev ? workspace_bytes : (size_t)0);
+    if (!aligned16(workspace_dev)) return fail(CPES_ERR_WORKSPACE, "%s: workspace must be 16-byte aligned", fn);
+    for (int32_t k = 0; k <= K; ++k)
+        offsets_host[k] = (int64_t)(((unsigned __int128)(uint64_t)d * (uint64_t)k + (uint64_t)K - 1u) / (uint64_t)K);
+    char* ws = static_cast<char*>(workspace_dev);
+    cpes::PartitionArgs a;
+    a.seed = seed;
+    a.d = d;
+    a.K = K;
+    a.half_bits = feistel_half_bits(d);
+    a.bucket = reinterpret_cast<uint8_t*>(ws);
+    a.counts = reinterpret_cast<uint32_t*>(ws + L.off_counts);
+    a.pos = reinterpret_cast<int64_t*>(ws + L.off_pos);
+    a.block_sums = reinterpret_cast<int64_t*>(ws + L.off_block_sums);
+    a.n_tiles = L.n_tiles;
+    a.index = index_dev;
+    a.status = status_dev;
+    return hip_status(cpes::launch_partition(a, (hipStream_t)stream), fn);
+}
+
+int cpes_perturb(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float sigma, uint64_t seed,
+                 int32_t sign, void* aux_dev, int aux_mode, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_perturb";
+    int rc = check_subspace(w_dev, numel, dtype, s, fn);
+    if (rc) return rc;
+    if ((rc = check_sign(sign, fn)) || (rc = check_sigma(sigma, fn))) return rc;
+    if (aux_mode != CPES_AUX_NONE && aux_mode != CPES_AUX_SNAPSHOT && aux_mode != CPES_AUX_MASTER)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown aux_mode %d", fn, aux_mode);
+    if (aux_mode != CPES_AUX_NONE && !aux_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: aux buffer is null", fn);
+    if (aux_mode == CPES_AUX_MASTER && dtype != CPES_BF16)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: master source needs bf16 weights", fn);
+    if (s->length == 0) return CPES_OK;
+    const float scale = sign > 0 ? sigma : -sigma;
+    const void* aux = aux_mode == CPES_AUX_NONE ? nullptr : aux_dev;
+    const bool vec = vector_ok(w_dev, dtype, s, aux, aux_mode == CPES_AUX_MASTER);
+    const cpes::StreamArgs a = stream_args(w_dev, numel, s, aux, seed, scale);
+    return hip_status(cpes::launch_perturb(dtype, aux_mode, s->index != nullptr, vec, a, (hipStream_t)stream), fn);
+}
+
+int cpes_restore(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float sigma, uint64_t seed,
+                 int32_t sign, const void* aux_dev, int aux_mode, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_restore";
+    int rc = check_subspace(w_dev, numel, dtype, s, fn);
+    if (rc) return rc;
+    if (aux_mode != CPES_AUX_NONE && aux_mode != CPES_AUX_SNAPSHOT && aux_mode != CPES_AUX_MASTER)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown aux_mode %d", fn, aux_mode);
+    if (aux_mode == CPES_AUX_NONE) {
+        if ((rc = check_sign(sign, fn)) || (rc = check_sigma(sigma, fn))) return rc;
+    } else if (!aux_dev) {
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: aux buffer is null", fn);
+    }
+    if (aux_mode == CPES_AUX_MASTER && dtype != CPES_BF16)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: master source needs bf16 weights", fn);
+    if (s->length == 0) return CPES_OK;
+    const bool gather = s->index != nullptr;
+    hipStream_t st = (hipStream_t)stream;
+    if (aux_mode == CPES_AUX_NONE) {
+        const float scale = sign > 0 ? -sigma : sigma;
+        const cpes::StreamArgs a = stream_args(w_dev, numel, s, nullptr, seed, scale);
+        return hip_status(cpes::launch_perturb(dtype, cpes::kAuxNone, gather, vector_ok(w_dev, dtype, s, nullptr, false), a, st), fn);
+    }
+    const cpes::StreamArgs a = stream_args(w_dev, numel, s, aux_dev, seed, 0.0f);
+    const bool vec = vector_ok(w_dev, dtype, s, aux_dev, aux_mode == CPES_AUX_MASTER);
+    if (aux_mode == CPES_AUX_SNAPSHOT) return hip_status(cpes::launch_restore_copy(dtype, gather, vec, a, st), fn);
+    return hip_status(cpes::launch_restore_master(gather, vec, a, st), fn);
+}
+
+int cpes_stage_master(const void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float* master_dev,
+                      void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_stage_master";
+    int rc = check_subspace(w_dev, numel, dtype, s, fn);
+    if (rc) return rc;
+    if (!master_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: master_dev is null", fn);
+    if (s->length == 0) return CPES_OK;
+    const bool vec = vector_ok(w_dev, dtype, s, master_dev, true);
+    const cpes::StreamArgs a = stream_args(const_cast<void*>(w_dev), numel, s, master_dev, 0, 0.0f);
+    return hip_status(cpes::launch_stage_master(dtype, s->index != nullptr, vec, a, (hipStream_t)stream), fn);
+}
+
+int cpes_normalize_rewards(const float* r_dev, int32_t n, int mode, const int32_t* group_dev, int32_t n_groups,
+                           float* out_dev, int32_t* status_dev, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_normalize_rewards";
+    if (!r_dev || !out_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: null reward or output pointer", fn);
+    if (n < 1 || n > CPES_MAX_REWARDS) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: n %d not in [1, %d]", fn, n, CPES_MAX_REWARDS);
+    if (mode != CPES_NORM_Z && mode != CPES_NORM_RANK) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown mode %d", fn, mode);
+    if (group_dev) {
+        if (n_groups < 1 || n_groups > n)
+            return fail(CPES_ERR_INVALID_ARGUMENT, "%s: n_groups %d not in [1, n]", fn, n_groups);
+        if (n_groups > CPES_MAX_GROUPS)
+            return fail(CPES_ERR_UNSUPPORTED, "%s: n_groups %d above CPES_MAX_GROUPS", fn, n_groups);
+    }
+    cpes::NormalizeArgs a;
+    a.r = r_dev;
+    a.group = group_dev;
+    a.out = out_dev;
+    a.status = status_dev;
+    a.n = n;
+    a.n_groups = group_dev ? n_groups : 1;
+    a.mode = mode;
+    return hip_status(cpes::launch_normalize(a, (hipStream_t)stream), fn);
+}
+
+int cpes_update(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float* master_dev, int32_t n,
+                const uint64_t* seeds_host, const int8_t* signs_host, const float* rnorm_dev, float alpha, float sigma,
+                int scale_mode, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_update";
+    int rc = check_subspace(w_dev, numel, dtype, s, fn);
+    if (rc) return rc;
+    if (n < 1) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: n %d < 1", fn, n);
+    if (n > CPES_MAX_MEMBERS) return fail(CPES_ERR_UNSUPPORTED, "%s: n %d above CPES_MAX_MEMBERS", fn, n);
+    if (!seeds_host || !signs_host || !rnorm_dev)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: null seeds, signs or rewards", fn);
+    if (scale_mode != CPES_SCALE_ALPHA_OVER_N_SIGMA && scale_mode != CPES_SCALE_ALPHA_OVER_N)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown scale_mode %d", fn, scale_mode);
+    if (!std::isfinite(alpha)) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: alpha is not finite", fn);
+    if (scale_mode == CPES_SCALE_ALPHA_OVER_N_SIGMA && (!std::isfinite(sigma) || sigma <= 0.0f))
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: sigma %g must be finite and > 0", fn, (double)sigma);
+    if (master_dev && dtype != CPES_BF16)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: a master copy needs bf16 weights", fn);
+    cpes::UpdateArgs a;
+    std::memset(&a, 0, sizeof a);
+    int n_streams = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        if ((rc = check_sign(signs_host[i], fn))) return rc;
+        int u = 0;
+        while (u < n_streams && ((uint64_t)a.seed_lo[u] | ((uint64_t)a.seed_hi[u] << 32)) != seeds_host[i]) ++u;
+        if (u == n_streams) {
+            a.seed_lo[u] = (uint32_t)seeds_host[i];
+            a.seed_hi[u] = (uint32_t)(seeds_host[i] >> 32);
+            ++n_streams;
+        }
+        a.member_stream[i] = (uint8_t)u;
+        a.member_sign[i] = signs_host[i];
+    }
+    if (s->length == 0) return CPES_OK;
+    const double step = scale_mode == CPES_SCALE_ALPHA_OVER_N_SIGMA ? (double)alpha / ((double)n * (double)sigma)
+                                                                    : (double)alpha / (double)n;
+    a.w = w_dev;
+    a.index = s->index;
+    a.master = master_dev;
+    a.rnorm = rnorm_dev;
+    a.offset = s->offset;
+    a.length = s->length;
+    a.numel = numel;
+    a.step = (float)step;
+    a.n_members = n;
+    a.n_streams = n_streams;
+    const bool vec = vector_ok(w_dev, dtype, s, master_dev, true);
+    return hip_status(cpes::launch_update(dtype, master_dev != nullptr, s->index != nullptr, vec, a, (hipStream_t)stream), fn);
+}
+
+int cpes_debug_philox(uint64_t seed, uint32_t domain, uint64_t q0, int64_t nblocks, uint32_t* out_dev, void* stream)
+{
+    g_error.clear();
+    if (!out_dev || nblocks < 0) return fail(CPES_ERR_INVALID_ARGUMENT, "cpes_debug_philox: bad output or count");
+    if (nblocks == 0) return CPES_OK;
+    return hip_status(cpes::launch_debug_philox(seed, domain, q0, nblocks, out_dev, (hipStream_t)stream), "cpes_debug_philox");
+}
+
+int cpes_debug_normals(uint64_t seed, int64_t j0, int64_t n, float* out_dev, void* stream)
+{
+    g_error.clear();
+    if (!out_dev || n < 0 || j0 < 0) return fail(CPES_ERR_INVALID_ARGUMENT, "cpes_debug_normals: bad output, j0 or count");
+    if (n == 0) return CPES_OK;
+    return hip_status(cpes::launch_debug_normals(seed, j0, n, out_dev, (hipStream_t)stream), "cpes_debug_normals");
+}
+
+int cpes_debug_bm_grid(uint32_t m0, int64_t n, double* rho_dev, double* cos_dev, double* sin_dev, void* stream)
+{
+    g_error.clear();
+    if (n < 0 || m0 < 1 || (int64_t)m0 + n - 1 > ((int64_t)1 << 24))
+        return fail(CPES_ERR_INVALID_ARGUMENT, "cpes_debug_bm_grid: grid outside [1, 2^24]");
+    if (n == 0) return CPES_OK;
+    return hip_status(cpes::launch_debug_bm_grid(m0, n, rho_dev, cos_dev, sin_dev, (hipStream_t)stream), "cpes_debug_bm_grid");
+}
+
+int cpes_debug_prp(uint64_t seed, int64_t d, int32_t K, int64_t i0, int64_t n, int64_t* perm_dev, int32_t* bucket_dev,
+                   void* stream)
+{
+    g_error.clear();
+    if (d < 1 || d >= ((int64_t)1 << 55) || K < 1 || K > CPES_MAX_PERMUTATION_K || (int64_t)K > d || i0 < 0 || n < 0 ||
+        i0 + n > d)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "cpes_debug_prp: bad d, K or range");
+    if (n == 0) return CPES_OK;
+    return hip_status(cpes::launch_debug_prp(seed, d, K, feistel_half_bits(d), i0, n, perm_dev, bucket_dev,
+                                             (hipStream_t)stream),
+                      "cpes_debug_prp");
+}
+
+int cpes_rng_probe(uint64_t seed, int64_t n, uint32_t* sink_dev, void* stream)
+{
+    g_error.clear();
+    if (!sink_dev || n < 0) return fail(CPES_ERR_INVALID_ARGUMENT, "cpes_rng_probe: bad sink or count");
+    return hip_status(cpes::launch_rng_probe(seed, n, sink_dev, (hipStream_t)stream), "cpes_rng_probe");
+}
+
+}  // extern "C"

@@ -1,0 +1,94 @@
+// cpes_launch.hpp -- argument blocks and launchers shared by the host runtime
+// (cpes_api.hip) and the kernels (cpes_kernels.hip).  Internal to the library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cpes {
+
+constexpr int kBlock = 256;             // threads per workgroup for streaming kernels
+constexpr int64_t kMaxGrid = 1 << 20;   // workgroups per launch; larger jobs loop
+
+// One subspace operation: positions j in [0, length) at parameter offset + j
+// or index[offset + j].
+struct StreamArgs {
+    void* w;
+    const int64_t* index;   // null: contiguous
+    void* aux;              // snapshot (dtype of w) or fp32 master, may be null
+    int64_t offset;
+    int64_t length;
+    int64_t numel;
+    uint32_t k0, k1;        // Philox key = member seed
+    float scale;            // +-sigma applied to the noise
+};
+
+enum AuxKind { kAuxNone = 0, kAuxSnapshot = 1, kAuxMaster = 2 };
+
+// Update: up to kMaxMembers members folded into up to kMaxMembers distinct
+// noise streams; all of it travels in the kernel argument block.
+constexpr int kMaxMembers = 256;
+
+struct UpdateArgs {
+    void* w;
+    const int64_t* index;
+    float* master;
+    const float* rnorm;
+    int64_t offset;
+    int64_t length;
+    int64_t numel;
+    float step;
+    int32_t n_members;
+    int32_t n_streams;
+    uint32_t seed_lo[kMaxMembers];
+    uint32_t seed_hi[kMaxMembers];
+    uint8_t member_stream[kMaxMembers];
+    int8_t member_sign[kMaxMembers];
+};
+
+struct NormalizeArgs {
+    const float* r;
+    const int32_t* group;
+    float* out;
+    int32_t* status;
+    int32_t n;
+    int32_t n_groups;
+    int32_t mode;
+};
+
+struct PartitionArgs {
+    uint64_t seed;
+    int64_t d;
+    int32_t K;
+    int32_t half_bits;      // h: the Feistel works on 2h bits
+    uint8_t* bucket;        // workspace: bucket of every element
+    uint32_t* counts;       // workspace: counts[k * n_tiles + tile]
+    int64_t* pos;           // workspace: exclusive positions, same layout
+    int64_t* block_sums;    // workspace: scan block partial sums
+    int64_t n_tiles;
+    int64_t* index;         // output map
+    int32_t* status;
+};
+
+// Tile of the permutation partition: one wave handles kTileItems x 64
+// consecutive elements.
+constexpr int kTileItems = 32;
+constexpr int64_t kTile = 64 * kTileItems;
+constexpr int kScanChunk = 4096;        // scan entries per workgroup
+
+hipError_t launch_perturb(int dtype, int aux, bool gather, bool vec, const StreamArgs& a, hipStream_t s);
+hipError_t launch_restore_copy(int dtype, bool gather, bool vec, const StreamArgs& a, hipStream_t s);
+hipError_t launch_restore_master(bool gather, bool vec, const StreamArgs& a, hipStream_t s);
+hipError_t launch_stage_master(int dtype, bool gather, bool vec, const StreamArgs& a, hipStream_t s);
+hipError_t launch_update(int dtype, bool master, bool gather, bool vec, const UpdateArgs& a, hipStream_t s);
+hipError_t launch_normalize(const NormalizeArgs& a, hipStream_t s);
+hipError_t launch_partition(const PartitionArgs& a, hipStream_t s);
+hipError_t launch_debug_philox(uint64_t seed, uint32_t domain, uint64_t q0, int64_t nblocks,
+                               uint32_t* out, hipStream_t s);
+hipError_t launch_debug_normals(uint64_t seed, int64_t j0, int64_t n, float* out, hipStream_t s);
+hipError_t launch_debug_bm_grid(uint32_t m0, int64_t n, double* rho, double* c, double* sn, hipStream_t s);
+hipError_t launch_debug_prp(uint64_t seed, int64_t d, int32_t K, int32_t half_bits, int64_t i0, int64_t n,
+                            int64_t* perm, int32_t* bucket, hipStream_t s);
+hipError_t launch_rng_probe(uint64_t seed, int64_t n, uint32_t* sink, hipStream_t s);
+
+}  // namespace cpes

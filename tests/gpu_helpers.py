@@ -1,0 +1,61 @@
+"""Helpers shared by the GPU tests: host/device conversions and ulp distances."""
+import numpy as np
+
+
+def torch():
+    import torch as _t
+
+    return _t
+
+
+def to_dev_bf16(bits: np.ndarray):
+    t = torch()
+    return t.from_numpy(np.ascontiguousarray(bits, dtype=np.uint16).view(np.int16)).view(t.bfloat16).cuda()
+
+
+def to_dev(a: np.ndarray):
+    t = torch()
+    if a.dtype == np.uint16:
+        return to_dev_bf16(a)
+    return t.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def to_host(x) -> np.ndarray:
+    t = torch()
+    if x.dtype == t.bfloat16:
+        return x.view(t.int16).cpu().numpy().view(np.uint16)
+    return x.cpu().numpy()
+
+
+def _ordered32(a: np.ndarray) -> np.ndarray:
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.int64)
+    neg = u >= 0x80000000
+    return np.where(neg, 0x80000000 - u, u)        # -0 and +0 both map to 0
+
+
+def ulp_f32(a, b) -> np.ndarray:
+    """Distance in fp32 ulps (units in the last place) between finite arrays."""
+    return np.abs(_ordered32(a) - _ordered32(b))
+
+
+def ulp_bf16(a_bits, b_bits) -> np.ndarray:
+    u = np.ascontiguousarray(a_bits, dtype=np.uint16).astype(np.int64)
+    v = np.ascontiguousarray(b_bits, dtype=np.uint16).astype(np.int64)
+    ou = np.where(u >= 0x8000, 0x8000 - u, u)
+    ov = np.where(v >= 0x8000, 0x8000 - v, v)
+    return np.abs(ou - ov)
+
+
+def normals_within_2ulp(got: np.ndarray, ref: np.ndarray) -> bool:
+    """|got - ref| <= 2 ulp32(ref), with ulp32(0) = 2^-149 (zeros must be exact)."""
+    got = got.astype(np.float64)
+    ref32 = ref.astype(np.float32)
+    ulp = np.where(ref32 == 0, 2.0 ** -149, np.spacing(np.abs(ref32)).astype(np.float64))
+    return bool(np.all(np.abs(got - ref.astype(np.float64)) <= 2 * ulp))
+
+
+def f32_close(got, ref, rtol=1e-5, atol=1e-7) -> bool:
+    """|got - ref| <= rtol |ref| + atol elementwise."""
+    g = got.astype(np.float64)
+    r = ref.astype(np.float64)
+    return bool(np.all(np.abs(g - r) <= rtol * np.abs(r) + atol))

@@ -1,0 +1,165 @@
+"""The C-ABI library loads without a GPU, exports every symbol include/cpes.h
+declares, and rejects bad arguments on the host (status code + message, before
+any HIP call).  No compute is launched here."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_02391_amd as cp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cpes.h")
+
+FAKE = 0x10000  # a non-null, 16-byte aligned address that is never dereferenced on these paths
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(cp.LIB_PATH):
+        pytest.fail("libcpes.so is not built (run __graft_entry__.build())")
+    return cp.load()
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^CPES_API\s+[\w\s\*]+?\b(cpes_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for required in ("cpes_partition", "cpes_perturb", "cpes_restore", "cpes_normalize_rewards", "cpes_update"):
+        assert required in names
+    assert sorted(cp.EXPORTED) == names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert lib.cpes_abi_version() == 1
+
+
+def _sub(offset=0, length=16, index=None):
+    return cp.Subspace(offset, length, index)
+
+
+def _rc_msg(lib, rc):
+    return rc, lib.cpes_last_error().decode()
+
+
+def test_perturb_rejects_bad_arguments(lib):
+    s = _sub()
+    cases = [
+        (None, 64, cp.BF16, ctypes.byref(s), 1e-3, 1, 1, None, cp.AUX_NONE),        # null weights
+        (FAKE, 64, 7, ctypes.byref(s), 1e-3, 1, 1, None, cp.AUX_NONE),              # bad dtype
+        (FAKE, 64, cp.BF16, None, 1e-3, 1, 1, None, cp.AUX_NONE),                   # null subspace
+        (FAKE, 64, cp.BF16, ctypes.byref(s), 1e-3, 1, 0, None, cp.AUX_NONE),        # sign 0
+        (FAKE, 64, cp.BF16, ctypes.byref(s), -1e-3, 1, 1, None, cp.AUX_NONE),       # sigma < 0
+        (FAKE, 64, cp.BF16, ctypes.byref(s), float("nan"), 1, 1, None, cp.AUX_NONE),
+        (FAKE, 64, cp.BF16, ctypes.byref(s), 1e-3, 1, 1, None, cp.AUX_SNAPSHOT),    # snapshot missing
+        (FAKE, 64, cp.BF16, ctypes.byref(s), 1e-3, 1, 1, FAKE, 9),                  # bad aux mode
+        (FAKE, 64, cp.F32, ctypes.byref(s), 1e-3, 1, 1, FAKE, cp.AUX_MASTER),       # master on fp32
+        (FAKE, 8, cp.BF16, ctypes.byref(s), 1e-3, 1, 1, None, cp.AUX_NONE),         # beyond numel
+        (FAKE, 64, cp.BF16, ctypes.byref(_sub(0, -1)), 1e-3, 1, 1, None, cp.AUX_NONE),
+        (FAKE, 64, cp.BF16, ctypes.byref(_sub(-4, 4)), 1e-3, 1, 1, None, cp.AUX_NONE),
+    ]
+    for args in cases:
+        rc, msg = _rc_msg(lib, lib.cpes_perturb(*args, None))
+        assert rc == cp.ERR_INVALID_ARGUMENT, args
+        assert msg.startswith("cpes_perturb:"), msg
+
+
+def test_empty_subspace_is_a_no_op(lib):
+    s = _sub(3, 0)
+    assert lib.cpes_perturb(FAKE, 64, cp.BF16, ctypes.byref(s), 1e-3, 1, 1, None, cp.AUX_NONE, None) == cp.OK
+    assert lib.cpes_restore(FAKE, 64, cp.BF16, ctypes.byref(s), 0.0, 0, 1, FAKE, cp.AUX_SNAPSHOT, None) == cp.OK
+    assert lib.cpes_last_error() == b""
+
+
+def test_restore_and_stage_reject_bad_arguments(lib):
+    s = _sub()
+    assert lib.cpes_restore(FAKE, 64, cp.BF16, ctypes.byref(s), 0.0, 0, 1, None, cp.AUX_SNAPSHOT, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_restore(FAKE, 64, cp.BF16, ctypes.byref(s), 1e-3, 0, 2, None, cp.AUX_NONE, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_restore(FAKE, 64, cp.F32, ctypes.byref(s), 0.0, 0, 1, FAKE, cp.AUX_MASTER, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_stage_master(FAKE, 64, cp.BF16, ctypes.byref(s), None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_stage_master(FAKE, 10, cp.BF16, ctypes.byref(s), FAKE, None) == cp.ERR_INVALID_ARGUMENT
+
+
+def test_normalize_rejects_bad_arguments(lib):
+    assert lib.cpes_normalize_rewards(None, 8, cp.NORM_Z, None, 1, FAKE, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_normalize_rewards(FAKE, 0, cp.NORM_Z, None, 1, FAKE, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_normalize_rewards(FAKE, 4097, cp.NORM_Z, None, 1, FAKE, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_normalize_rewards(FAKE, 8, 5, None, 1, FAKE, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_normalize_rewards(FAKE, 8, cp.NORM_Z, FAKE, 9, FAKE, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_normalize_rewards(FAKE, 2000, cp.NORM_Z, FAKE, 1500, FAKE, None, None) == cp.ERR_UNSUPPORTED
+
+
+def test_update_rejects_bad_arguments(lib):
+    s = _sub()
+    seeds = (ctypes.c_uint64 * 4)(1, 2, 3, 4)
+    signs = (ctypes.c_int8 * 4)(1, 1, -1, 1)
+    bad_signs = (ctypes.c_int8 * 4)(1, 0, -1, 1)
+    many = (ctypes.c_uint64 * 300)()
+    many_s = (ctypes.c_int8 * 300)(*([1] * 300))
+    args = lambda **kw: [kw.get("w", FAKE), 64, kw.get("dtype", cp.BF16), ctypes.byref(s), kw.get("master", None),
+                         kw.get("n", 4), kw.get("seeds", seeds), kw.get("signs", signs), kw.get("r", FAKE),
+                         kw.get("alpha", 5e-4), kw.get("sigma", 1e-3), kw.get("scale", 0), None]
+    assert lib.cpes_update(*args(w=None)) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_update(*args(n=0)) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_update(*args(n=300, seeds=many, signs=many_s)) == cp.ERR_UNSUPPORTED
+    assert lib.cpes_update(*args(signs=bad_signs)) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_update(*args(r=None)) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_update(*args(sigma=0.0)) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_update(*args(alpha=float("inf"))) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_update(*args(scale=3)) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_update(*args(dtype=cp.F32, master=FAKE)) == cp.ERR_INVALID_ARGUMENT
+    assert "cpes_update" in lib.cpes_last_error().decode()
+
+
+def test_partition_host_paths(lib):
+    off = (ctypes.c_int64 * 4)()
+    assert lib.cpes_partition(cp.PART_CONTIGUOUS, 10, 3, 0, None, off, None, None, 0, None, None) == cp.OK
+    assert list(off) == [0, 3, 6, 10]
+    b = (ctypes.c_int64 * 4)(0, 4, 4, 10)
+    assert lib.cpes_partition(cp.PART_CONTIGUOUS, 10, 3, 0, b, off, None, None, 0, None, None) == cp.OK
+    assert list(off) == [0, 4, 4, 10]
+    bad = (ctypes.c_int64 * 4)(0, 5, 4, 10)
+    assert lib.cpes_partition(cp.PART_CONTIGUOUS, 10, 3, 0, bad, off, None, None, 0, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_partition(cp.PART_CONTIGUOUS, 10, 11, 0, None, off, None, None, 0, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_partition(7, 10, 3, 0, None, off, None, None, 0, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_partition(cp.PART_PERMUTATION, 10, 300, 0, None, (ctypes.c_int64 * 301)(), FAKE, FAKE, 1 << 20,
+                              None, None) == cp.ERR_INVALID_ARGUMENT  # K > d
+    assert lib.cpes_partition(cp.PART_PERMUTATION, 1000, 300, 0, None, (ctypes.c_int64 * 301)(), FAKE, FAKE,
+                              1 << 20, None, None) == cp.ERR_UNSUPPORTED
+    need = lib.cpes_partition_workspace_bytes(cp.PART_PERMUTATION, 1000, 8)
+    assert need >= 1000
+    assert lib.cpes_partition(cp.PART_PERMUTATION, 1000, 8, 0, None, (ctypes.c_int64 * 9)(), FAKE, FAKE, need - 1,
+                              None, None) == cp.ERR_WORKSPACE
+    assert lib.cpes_partition(cp.PART_PERMUTATION, 1000, 8, 0, None, (ctypes.c_int64 * 9)(), None, FAKE, need,
+                              None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_partition_workspace_bytes(cp.PART_CONTIGUOUS, 1000, 8) == 0
+    assert lib.cpes_partition_workspace_bytes(cp.PART_PERMUTATION, 1000, 0) == 0
+
+
+def test_debug_hooks_reject_bad_arguments(lib):
+    assert lib.cpes_debug_philox(0, 0, 0, -1, FAKE, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_debug_normals(0, -1, 4, FAKE, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_debug_bm_grid(0, 4, None, None, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_debug_bm_grid(1 << 24, 2, None, None, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_debug_prp(0, 100, 8, 90, 20, None, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_rng_probe(0, 8, None, None) == cp.ERR_INVALID_ARGUMENT
+
+
+def test_binding_raises_without_fallback(tmp_path):
+    """A missing library is an error, never a silent CPU path."""
+    import importlib
+
+    mod = importlib.import_module("paper_2608_02391_amd")
+    saved = mod._lib
+    try:
+        mod._lib = None
+        with pytest.raises(RuntimeError):
+            mod.load(str(tmp_path / "missing.so"))
+    finally:
+        mod._lib = saved

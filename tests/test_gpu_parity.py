@@ -1,0 +1,330 @@
+"""GPU parity: every entry point of libcpes (called through the C ABI) against
+the CPU oracle, element by element, on the same seeded inputs.  Sizes span many
+workgroups and a ragged tail; offsets include unaligned ones; index-map
+(gather/scatter) subspaces come from the oracle's own partition.
+
+Tolerances: Philox words, index maps, snapshots and restores bit-exact;
+normals within 2 fp32 ulp; bf16 results within 1 bf16 ulp; fp32 results within
+1e-5 relative + 1e-7 absolute."""
+import functools
+
+import numpy as np
+import pytest
+
+import paper_2608_02391_amd as cp
+import synthetic as S
+from tests.gpu_helpers import (f32_close, normals_within_2ulp, to_dev, to_host, torch, ulp_bf16, ulp_f32)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def T():
+    t = torch()
+    assert t.cuda.is_available(), "GPU tests need an MI355X"
+    cp.load()
+    return t
+
+
+def _sync(T):
+    T.cuda.synchronize()
+
+
+# ------------------------------------------------------------------ Philox --
+
+@pytest.mark.parametrize("seed,domain,q0,nb", [
+    (0, 0, 0, 1 << 16),
+    (33, 3, (5 << 32) - 100, 4096),          # crosses the hi word of the counter
+    (2**64 - 1, 0, 2**40 + 7, 1000),
+    (123456789012345, 2, 17, 77777),
+])
+def test_philox_streams_bit_exact(orc, T, seed, domain, q0, nb):
+    out = T.empty(4 * nb, dtype=T.int32, device="cuda")
+    cp.cpes_debug_philox(seed, domain, q0, nb, out)
+    got = to_host(out).view(np.uint32)
+    ref = orc.blocks(seed, domain, q0, nb)
+    assert np.array_equal(got, ref)
+
+
+# -------------------------------------------------------------- transform --
+
+def test_box_muller_halves_exhaustive(orc, T):
+    """Radius and angle on the whole 2^24-point uniform grid against the oracle."""
+    n = 1 << 24
+    rho = T.empty(n, dtype=T.float64, device="cuda")
+    c = T.empty(n, dtype=T.float64, device="cuda")
+    s = T.empty(n, dtype=T.float64, device="cuda")
+    cp.cpes_debug_bm_grid(1, n, rho, c, s)
+    words = ((np.arange(1, n + 1, dtype=np.uint64) - 1) << 8).astype(np.uint32)
+    r_ref = orc.bm_radius_many(words)
+    c_ref, s_ref = orc.bm_angle_many(words)
+    g_rho, g_c, g_s = to_host(rho), to_host(c), to_host(s)
+    for got, ref in ((g_rho, r_ref), (g_c, c_ref), (g_s, s_ref)):
+        zero = ref == 0
+        assert np.all(got[zero] == 0)
+        rel = np.abs(got[~zero] - ref[~zero]) / np.abs(ref[~zero])
+        assert rel.max() < 2.0 ** -40, rel.max()
+
+
+@pytest.mark.parametrize("seed,j0,n", [
+    (1, 0, (1 << 20) + 3),
+    (2**33 + 5, 3, 100001),
+    (2**64 - 1, (1 << 34) - 6, 4099),         # block index crosses 2^32
+    (7, 1, 1),
+])
+def test_normals_within_two_ulp(orc, T, seed, j0, n):
+    out = T.empty(n, dtype=T.float32, device="cuda")
+    cp.cpes_debug_normals(seed, j0, n, out)
+    got = to_host(out)
+    ref = orc.normals(seed, j0, n)
+    assert normals_within_2ulp(got, ref)
+    assert np.mean(got == ref) > 0.999
+
+
+def test_gpu_normal_statistics(T):
+    n = 1 << 26
+    out = T.empty(n, dtype=T.float32, device="cuda")
+    cp.cpes_debug_normals(11, 0, n, out)
+    z = out.double()
+    se = 1.0 / np.sqrt(n)
+    assert abs(z.mean().item()) < 5 * se
+    assert abs(z.var(unbiased=False).item() - 1.0) < 5 * np.sqrt(2.0) * se
+    assert abs(((z - z.mean()) ** 3).mean().item()) < 5 * np.sqrt(15.0) * se
+    assert abs(((z - z.mean()) ** 4).mean().item() - 3.0) < 5 * np.sqrt(96.0) * se
+
+
+# ------------------------------------------------------------ perturb etc --
+
+LAYOUTS = ["aligned", "unaligned", "gather"]
+LENGTHS = [1, 7, 9, 4095, (1 << 20) + 5]
+
+
+@functools.lru_cache(maxsize=None)
+def _perm_partition(d):
+    import oracle as O
+
+    return O.partition(O.PART_PERMUTATION, d, 4, seed=33)
+
+
+def _layout(layout, length):
+    """(numel, offset, host index map or None) for a subspace of `length`:
+    a contiguous range at an aligned or unaligned offset, or subspace 1 of a
+    4-way permutation partition of 4 * length indices (its map starts at an
+    offset that is not a multiple of the vector width)."""
+    if layout == "aligned":
+        return length + 64, 16, None
+    if layout == "unaligned":
+        return length + 64, 3, None
+    d = max(4 * length, 8)
+    offsets, index = _perm_partition(d)
+    assert offsets[2] - offsets[1] >= length
+    return d, int(offsets[1]), index
+
+
+def _setup(orc, T, dtype, layout, length, wseed):
+    numel, offset, index = _layout(layout, length)
+    w = S.host_weights(numel, dtype, wseed)
+    return w, to_dev(w), offset, index, (to_dev(index) if index is not None else None)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("length", LENGTHS)
+@pytest.mark.parametrize("dtype,aux", [(S.BF16, 0), (S.BF16, 1), (S.BF16, 2), (S.F32, 0), (S.F32, 1)])
+def test_perturb_matches_oracle(orc, T, dtype, aux, layout, length):
+    w, dw, off, index, dindex = _setup(orc, T, dtype, layout, length, 1000 + length)
+    sigma, seed, sign = np.float32(2.8284e-3), 17 + length, (-1 if length % 2 else 1)
+    w0 = w.copy()
+    snap_h = snap_d = master_h = master_d = None
+    if aux == 1:
+        snap_h = np.zeros(length, dtype=w.dtype)
+        snap_d = to_dev(snap_h)
+    if aux == 2:
+        master_h = S.host_weights(length, S.F32, 7 + length)
+        master_d = to_dev(master_h)
+    s = cp.subspace(off, length, dindex)
+    cp.cpes_perturb(dw, s, float(sigma), seed, sign, aux=snap_d if aux == 1 else master_d, aux_mode=aux)
+    orc.perturb(w, off, length, sigma, seed, sign, index=index, aux=snap_h if aux == 1 else master_h, aux_mode=aux)
+    _sync(T)
+    got = to_host(dw)
+    touched = np.zeros(w.size, dtype=bool)
+    pos = index[off:off + length] if index is not None else np.arange(off, off + length)
+    touched[pos] = True
+    assert np.array_equal(got[~touched], w0[~touched])              # outside: bitwise untouched
+    if dtype == S.BF16:
+        assert ulp_bf16(got[touched], w[touched]).max() <= 1
+    else:
+        assert f32_close(got[touched], w[touched])
+        assert ulp_f32(got[touched], w[touched]).max() <= 1
+    if aux == 1:
+        assert np.array_equal(to_host(snap_d), snap_h)              # the backup is exact
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("dtype", [S.BF16, S.F32])
+def test_snapshot_and_master_restore_are_identities(orc, T, dtype, layout):
+    length = (1 << 20) + 5
+    w, dw, off, index, dindex = _setup(orc, T, dtype, layout, length, 5)
+    s = cp.subspace(off, length, dindex)
+    snap = T.empty(length, dtype=dw.dtype, device="cuda")
+    cp.cpes_perturb(dw, s, 4e-3, 99, 1, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+    _sync(T)
+    assert not np.array_equal(to_host(dw), w)
+    cp.cpes_restore(dw, s, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+    _sync(T)
+    assert np.array_equal(to_host(dw), w)
+    if dtype == S.BF16:
+        master = T.empty(length, dtype=T.float32, device="cuda")
+        cp.cpes_stage_master(dw, s, master)
+        pos = index[off:off + length] if index is not None else np.arange(off, off + length)
+        _sync(T)
+        assert np.array_equal(to_host(master), orc.bf16_to_f32(w[pos]))  # staging is exact
+        cp.cpes_perturb(dw, s, 4e-3, 5, -1, aux=master, aux_mode=cp.AUX_MASTER)
+        cp.cpes_restore(dw, s, aux=master, aux_mode=cp.AUX_MASTER)
+        _sync(T)
+        assert np.array_equal(to_host(dw), w)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("dtype", [S.BF16, S.F32])
+def test_replay_restore_matches_oracle(orc, T, dtype, layout):
+    length = 300007
+    w, dw, off, index, dindex = _setup(orc, T, dtype, layout, length, 6)
+    s = cp.subspace(off, length, dindex)
+    cp.cpes_perturb(dw, s, 2e-3, 3, -1)
+    cp.cpes_restore(dw, s, 2e-3, 3, -1, aux=None, aux_mode=cp.AUX_NONE)
+    orc.perturb(w, off, length, np.float32(2e-3), 3, -1, index=index)
+    orc.restore(w, off, length, np.float32(2e-3), 3, -1, index=index)
+    _sync(T)
+    got = to_host(dw)
+    if dtype == S.BF16:
+        assert ulp_bf16(got, w).max() <= 1
+    else:
+        assert f32_close(got, w)
+
+
+# --------------------------------------------------------------- normalise --
+
+@pytest.mark.parametrize("n", [1, 2, 8, 30, 32, 40, 128, 1000, 4096])
+@pytest.mark.parametrize("mode", [S.NORM_Z, S.NORM_RANK])
+@pytest.mark.parametrize("kind", ["uniform", "bernoulli", "mean_bernoulli"])
+def test_normalize_matches_oracle(orc, T, n, mode, kind):
+    r = S.rewards(kind, n, 99 + n)
+    out = T.empty(n, dtype=T.float32, device="cuda")
+    st = T.full((1,), -7, dtype=T.int32, device="cuda")
+    cp.cpes_normalize_rewards(to_dev(r), out, mode, status=st)
+    ref, rst = orc.normalize(r, mode)
+    _sync(T)
+    assert int(st.item()) == rst == 0
+    assert np.array_equal(to_host(out), ref)
+
+
+@pytest.mark.parametrize("mode", [S.NORM_Z, S.NORM_RANK])
+def test_normalize_grouped_and_failures(orc, T, mode):
+    n, K = 40, 4
+    r = S.rewards("uniform", n, 12)
+    g = np.repeat(np.arange(K), n // K).astype(np.int32)[np.random.default_rng(2).permutation(n)]
+    out = T.empty(n, dtype=T.float32, device="cuda")
+    st = T.zeros(1, dtype=T.int32, device="cuda")
+    cp.cpes_normalize_rewards(to_dev(r), out, mode, group=to_dev(g), n_groups=K, status=st)
+    ref, _ = orc.normalize(r, mode, g)
+    _sync(T)
+    assert np.array_equal(to_host(out), ref) and int(st.item()) == 0
+    # constant rewards -> zeros; a NaN -> zeros + status 1; a bad group id -> zeros + status 2
+    cp.cpes_normalize_rewards(to_dev(np.full(n, 0.5, np.float32)), out, mode, status=st)
+    _sync(T)
+    assert np.all(to_host(out) == 0) and int(st.item()) == 0
+    rr = r.copy()
+    rr[7] = np.nan
+    cp.cpes_normalize_rewards(to_dev(rr), out, mode, status=st)
+    _sync(T)
+    assert np.all(to_host(out) == 0) and int(st.item()) == 1
+    gg = g.copy()
+    gg[3] = K
+    cp.cpes_normalize_rewards(to_dev(r), out, mode, group=to_dev(gg), n_groups=K, status=st)
+    _sync(T)
+    assert np.all(to_host(out) == 0) and int(st.item()) == 2
+
+
+# ------------------------------------------------------------------ update --
+
+MEMBER_SETS = {
+    "one": ([5], [1]),
+    "pairs4": ([9, 9, 12, 40], [1, -1, 1, 1]),
+    "n30": (list(range(1, 31)), [1] * 30),
+    "n128_antithetic": ([s for s in range(1001, 1065) for _ in (0, 1)], [1, -1] * 64),
+}
+
+
+@pytest.mark.parametrize("members", list(MEMBER_SETS))
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("kind", ["bf16", "f32", "master"])
+def test_update_matches_oracle(orc, T, kind, layout, members):
+    seeds, signs = MEMBER_SETS[members]
+    n = len(seeds)
+    length = (1 << 18) + 5 if n > 30 else (1 << 20) + 3
+    dtype = S.F32 if kind == "f32" else S.BF16
+    w, dw, off, index, dindex = _setup(orc, T, dtype, layout, length, 20 + n)
+    r = S.rewards("uniform", n, 7 + n)
+    rnorm, _ = orc.normalize(r, S.NORM_Z)
+    scale = S.SCALE_ALPHA_OVER_N if members == "pairs4" else S.SCALE_ALPHA_OVER_N_SIGMA
+    alpha, sigma = np.float32(5e-4), np.float32(2.25e-3)
+    s = cp.subspace(off, length, dindex)
+    master_h = master_d = None
+    if kind == "master":
+        pos = index[off:off + length] if index is not None else np.arange(off, off + length)
+        master_h = orc.bf16_to_f32(w[pos]).copy()
+        master_d = to_dev(master_h)
+    w0 = w.copy()
+    cp.cpes_update(dw, s, seeds, signs, to_dev(rnorm), float(alpha), float(sigma), scale, master=master_d)
+    orc.update(w, off, length, seeds, signs, rnorm, alpha, sigma, scale, index=index, master=master_h)
+    _sync(T)
+    got = to_host(dw)
+    changed = np.zeros(w.size, dtype=bool)
+    pos = index[off:off + length] if index is not None else np.arange(off, off + length)
+    changed[pos] = True
+    assert np.array_equal(got[~changed], w0[~changed])
+    if dtype == S.BF16:
+        assert ulp_bf16(got, w).max() <= 1
+    else:
+        assert f32_close(got, w)
+    if kind == "master":
+        assert f32_close(to_host(master_d), master_h)
+
+
+def test_update_mirrored_equal_rewards_is_identity(T):
+    w = S.host_weights(100003, S.BF16, 3)
+    dw = to_dev(w)
+    rn = to_dev(np.array([0.7, 0.7, -1.1, -1.1], np.float32))
+    cp.cpes_update(dw, cp.subspace(0, 100003), [4, 4, 8, 8], [1, -1, 1, -1], rn, 5e-4, 4e-3)
+    _sync(T)
+    assert np.array_equal(to_host(dw), w)
+
+
+# --------------------------------------------------------------- partition --
+
+@pytest.mark.parametrize("d,K", [(1, 1), (2, 2), (7, 3), (1000, 8), (4096, 4), (100003, 8), ((1 << 20) + 3, 256),
+                                 ((1 << 21) + 1, 16)])
+def test_permutation_partition_bit_exact(orc, T, d, K):
+    ws = T.empty(cp.cpes_partition_workspace_bytes(cp.PART_PERMUTATION, d, K), dtype=T.uint8, device="cuda")
+    index = T.full((d,), -1, dtype=T.int64, device="cuda")
+    st = T.full((1,), -7, dtype=T.int32, device="cuda")
+    offsets = cp.cpes_partition(cp.PART_PERMUTATION, d, K, seed=33, index=index, workspace=ws, status=st)
+    ref_off, ref_index = orc.partition(orc.PART_PERMUTATION, d, K, seed=33)
+    _sync(T)
+    assert offsets == [int(x) for x in ref_off]
+    assert int(st.item()) == 0
+    assert np.array_equal(to_host(index), ref_index)
+
+
+def test_prp_values_bit_exact(orc, T):
+    for d, K in ((4022468096, 8), (1 << 20, 4), (12345, 7)):
+        i0 = max(0, d - 5000)
+        n = min(d, 5000)
+        perm = T.empty(n, dtype=T.int64, device="cuda")
+        bucket = T.empty(n, dtype=T.int32, device="cuda")
+        cp.cpes_debug_prp(33, d, K, i0, n, perm, bucket)
+        _sync(T)
+        p, b = to_host(perm), to_host(bucket)
+        for k in range(0, n, 37):
+            assert p[k] == orc.prp(33, d, i0 + k)
+            assert b[k] == orc.bucket(33, d, K, i0 + k)
