@@ -810,8 +810,10 @@ hipError_t launch_debug_prp(uint64_t seed, int64_t d, int32_t K, int32_t half_bi
 
 hipError_t launch_rng_probe(uint64_t seed, int64_t n, uint32_t* sink, hipStream_t s)
 {
+    // A few workgroups per CU looping over the units: one atomic per wave.
+    const int64_t blocks = grid_for((n + 7) / 8) < 8192 ? grid_for((n + 7) / 8) : 8192;
     hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(1), 0, s, sink);
-    hipLaunchKernelGGL(k_rng_probe, dim3((unsigned)grid_for((n + 7) / 8)), dim3(kBlock), 0, s, seed, n, sink);
+    hipLaunchKernelGGL(k_rng_probe, dim3((unsigned)blocks), dim3(kBlock), 0, s, seed, n, sink);
     return hipGetLastError();
 }
 

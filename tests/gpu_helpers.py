@@ -59,3 +59,30 @@ def f32_close(got, ref, rtol=1e-5, atol=1e-7) -> bool:
     g = got.astype(np.float64)
     r = ref.astype(np.float64)
     return bool(np.all(np.abs(g - r) <= rtol * np.abs(r) + atol))
+
+
+def bf16_value(bits) -> np.ndarray:
+    return (np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def bf16_ulp(x: np.ndarray) -> np.ndarray:
+    """Spacing of bf16 numbers at |x| (8 significand bits)."""
+    ax = np.abs(x.astype(np.float64))
+    _, e = np.frexp(np.where(ax == 0, 2.0 ** -126, ax))
+    return np.ldexp(1.0, e - 8)
+
+
+def bf16_close(got_bits, ref_bits, atol=1e-7) -> bool:
+    """|got - ref| <= 1 bf16 ulp(ref) + atol.  The absolute term covers results
+    that cancel to near zero, where a bf16 ulp is far below the fp32
+    accumulation error of a many-member update."""
+    g = bf16_value(got_bits).astype(np.float64)
+    r = bf16_value(ref_bits).astype(np.float64)
+    return bool(np.all(np.abs(g - r) <= bf16_ulp(r) + atol))
+
+
+def describe_mismatch(got, ref) -> str:
+    g = got.astype(np.float64)
+    r = ref.astype(np.float64)
+    k = int(np.argmax(np.abs(g - r)))
+    return f"max |diff| {abs(g[k] - r[k]):.3e} at {k}: got {g[k]!r} ref {r[k]!r}"
