@@ -1,0 +1,276 @@
+"""Benchmark of the CoPES parameter-space hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload c3]
+
+One step = one pass of the hot path over every subspace of the workload:
+for each active subspace: partition lookup, N x (perturb with backup, restore),
+reward normalisation, seed-replayed update.  Inputs (weights, rewards) are
+resident in HBM before the timed region.  Prints ONE JSON line.
+
+Workloads (synthetic, see synthetic/__init__.py): c3 (default; 4,022,468,096
+bf16 params, 8 layer-group subspaces, N = 30), c1, c2, c4 (index-map
+subspaces), c5 (fp32 master, 16 iterations of N = 128).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "GB/s and % HBM peak for perturb/restore + ES update (params/s) at 4B params"
+HBM_PEAK_GBPS = 8000.0                 # MI355X HBM3E
+VALU_LANE_OPS_PEAK = 256 * 64 * 2.4e9  # 256 CUs x 64 lanes x 2.4 GHz: one VALU lane-op per lane per clock
+# VALU instructions per normal of the perturb kernel (SQ_INSTS_VALU per
+# dispatch / normals per dispatch, bf16 with snapshot; see profiles/).
+VALU_INSTS_PER_NORMAL = 66.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=3)
+    p.add_argument("--warmup", type=int, default=1)
+    p.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-positions", type=int, default=1 << 23,
+                   help="positions per subspace sample for the oracle baseline")
+    return p.parse_args()
+
+
+class KernelTimer:
+    """HIP-event timing of each launch of a kernel class on the working stream."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.pending = {}
+        self.done = {}
+
+    def run(self, name, fn):
+        ev0 = self.torch.cuda.Event(enable_timing=True)
+        ev1 = self.torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        fn()
+        ev1.record()
+        self.pending.setdefault(name, []).append((ev0, ev1))
+
+    def collect(self):
+        for name, evs in self.pending.items():
+            self.done.setdefault(name, []).extend(a.elapsed_time(b) for a, b in evs)
+        self.pending = {}
+
+    def stats(self, name):
+        ts = self.done.get(name, [])
+        return (sum(ts) / len(ts) if ts else 0.0), len(ts), sum(ts)
+
+
+def build_plan(W, cp, torch):
+    """Device buffers and the per-step call sequence of workload W."""
+    import numpy as np
+
+    import synthetic as S
+
+    dev = torch.device("cuda")
+    w = S.device_weights(W.d, W.dtype, W.weight_seed)
+    sizes = W.sizes()
+    index = ws = None
+    if W.partition_mode == S.PART_PERMUTATION:
+        index = torch.empty(W.d, dtype=torch.int64, device=dev)
+        ws = torch.empty(cp.cpes_partition_workspace_bytes(cp.PART_PERMUTATION, W.d, W.K), dtype=torch.uint8,
+                         device=dev)
+    maxk = max(sizes[k] for k in W.active)
+    tdt = torch.bfloat16 if W.dtype == S.BF16 else torch.float32
+    aux = torch.empty(maxk, dtype=torch.float32 if W.master else tdt, device=dev)
+    n_iter = len(W.active)
+    rewards = torch.from_numpy(np.stack([W.rewards(t) for t in range(n_iter)])).to(dev)
+    rnorm = torch.empty_like(rewards)
+    return dict(w=w, index=index, ws=ws, aux=aux, rewards=rewards, rnorm=rnorm, sizes=sizes)
+
+
+def run_step(W, cp, torch, P, timer, offsets_cache):
+    import synthetic as S
+
+    if W.partition_mode == S.PART_PERMUTATION:
+        if "perm" not in offsets_cache:   # partition is timed on its own (a one-off per ES step)
+            offsets_cache["perm"] = cp.cpes_partition(cp.PART_PERMUTATION, W.d, W.K, W.partition_seed,
+                                                      index=P["index"], workspace=P["ws"])
+        offsets = offsets_cache["perm"]
+    else:
+        offsets = cp.cpes_partition(cp.PART_CONTIGUOUS, W.d, W.K, bounds=W.bounds)
+    aux_mode = cp.AUX_MASTER if W.master else cp.AUX_SNAPSHOT
+    for t, k in enumerate(W.active):
+        length = offsets[k + 1] - offsets[k]
+        s = cp.subspace(offsets[k], length, P["index"])
+        sigma = W.sigma_k(k)
+        seeds = W.member_seeds(t)
+        aux = P["aux"][:length]
+        if W.master:
+            timer.run("stage_master", lambda: cp.cpes_stage_master(P["w"], s, aux))
+        for seed, sign in zip(seeds, W.signs):
+            timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigma, seed, sign, aux=aux, aux_mode=aux_mode))
+            # (the perturbed model would be evaluated here)
+            timer.run("restore", lambda: cp.cpes_restore(P["w"], s, aux=aux, aux_mode=aux_mode))
+        timer.run("normalize", lambda: cp.cpes_normalize_rewards(P["rewards"][t], P["rnorm"][t], W.norm_mode))
+        timer.run("update", lambda: cp.cpes_update(P["w"], s, seeds, W.signs, P["rnorm"][t], W.alpha, sigma,
+                                                   W.scale_mode, master=aux if W.master else None))
+
+
+def bytes_per_position(W, op):
+    """Algorithmic HBM bytes per subspace position."""
+    import synthetic as S
+
+    e = 2 if W.dtype == S.BF16 else 4
+    ix = 8 if W.partition_mode == S.PART_PERMUTATION else 0
+    if op == "perturb":
+        return (4 + e if W.master else 3 * e) + ix      # read w (or master), write w (+ snapshot)
+    if op == "restore":
+        return (4 + e if W.master else 2 * e) + ix
+    if op == "update":
+        return (4 + 4 + e if W.master else 2 * e) + ix
+    if op == "stage_master":
+        return e + 4 + ix
+    return 0
+
+
+def cpu_baseline(W, positions):
+    """The oracle on a bounded sample: the first `positions` positions of every
+    active subspace, every member (perturb with backup, restore) and the
+    update; extrapolated linearly to the full step."""
+    import numpy as np
+
+    import oracle as O
+    import synthetic as S
+
+    O.build(force=False)
+    sizes = W.sizes()
+    t_total, pos_total, full_total = 0.0, 0, 0
+    for t, k in enumerate(W.active[:2]):
+        n = min(positions, sizes[k])
+        w = S.host_weights(n, W.dtype, 1 + k)
+        seeds = W.member_seeds(t)
+        aux = np.empty(n, dtype=np.float32 if W.master else w.dtype)
+        mode = O.AUX_MASTER if W.master else O.AUX_SNAPSHOT
+        rn, _ = O.normalize(W.rewards(t), W.norm_mode)
+        t0 = time.perf_counter()
+        if W.master:
+            aux[:] = O.stage_master(w, 0, n)
+        for seed, sign in zip(seeds, W.signs):
+            O.perturb(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=mode)
+            O.restore(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=mode)
+        O.normalize(W.rewards(t), W.norm_mode)
+        O.update(w, 0, n, seeds, W.signs, rn, np.float32(W.alpha), np.float32(W.sigma_k(k)), W.scale_mode,
+                 master=aux if W.master else None)
+        t_total += time.perf_counter() - t0
+        pos_total += n
+    full_total = sum(sizes[k] for k in W.active)
+    step_s = t_total / pos_total * full_total
+    return {"value": W.d / step_s, "unit": "params/s", "cores": O.num_threads(), "kind": "oracle",
+            "sample": f"first {positions} positions of subspaces {list(W.active[:2])}, all {W.n} members "
+                      f"(perturb+backup, restore) + normalise + update; {t_total:.1f} s, "
+                      f"extrapolated per position to the full step"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU "
+              "path, see DESIGN.md for how it would shard.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2608_02391_amd as cp
+    import synthetic as S
+
+    W = S.workload(args.workload)
+    cp.load()
+    torch.cuda.set_device(0)
+    P = build_plan(W, cp, torch)
+    torch.cuda.synchronize()
+    cache = {}
+    part_ms = None
+    if W.partition_mode == S.PART_PERMUTATION:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        cache["perm"] = cp.cpes_partition(cp.PART_PERMUTATION, W.d, W.K, W.partition_seed, index=P["index"],
+                                          workspace=P["ws"])
+        e1.record()
+        torch.cuda.synchronize()
+        part_ms = e0.elapsed_time(e1)
+    warm = KernelTimer(torch)
+    for _ in range(args.warmup):
+        run_step(W, cp, torch, P, warm, cache)
+    torch.cuda.synchronize()
+    timer = KernelTimer(torch)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        run_step(W, cp, torch, P, timer, cache)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    timer.collect()
+    ms_step = elapsed * 1e3 / args.steps
+
+    sizes = W.sizes()
+    span = sum(sizes[k] for k in W.active)                # subspace positions visited per step
+    ops = {}
+    for op in ("perturb", "restore", "update", "normalize", "stage_master"):
+        avg_ms, count, tot_ms = timer.stats(op)
+        if count == 0:
+            continue
+        per_step = span * (W.n if op in ("perturb", "restore") else 1)
+        per_launch = per_step / (count / args.steps)     # average positions per launch
+        entry = {"launches": count, "avg_ms": round(avg_ms, 4), "ms_per_step": round(tot_ms / args.steps, 3),
+                 "positions_per_launch": round(per_launch)}
+        b = bytes_per_position(W, op)
+        if b:
+            gbps = b * per_launch / (avg_ms * 1e-3) / 1e9
+            entry["GB/s"] = round(gbps, 1)
+            entry["frac_hbm"] = round(gbps / HBM_PEAK_GBPS, 4)
+        if op in ("perturb", "update"):
+            streams = len(set(W.member_seeds(0))) if op == "update" else 1
+            entry["params/s"] = round(per_launch / (avg_ms * 1e-3), 1)
+            entry["Gnormal/s"] = round(streams * per_launch / (avg_ms * 1e-3) / 1e9, 2)
+        ops[op] = entry
+    dominant = max((o for o in ops if o != "normalize"), key=lambda o: ops[o]["ms_per_step"])
+    d_entry = ops[dominant]
+    if dominant == "restore" or dominant == "stage_master":
+        roof = {"bound": "hbm", "achieved": d_entry["GB/s"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(d_entry["GB/s"] / HBM_PEAK_GBPS, 4), "traffic": None}
+    else:
+        peak_gn = VALU_LANE_OPS_PEAK / VALU_INSTS_PER_NORMAL / 1e9
+        roof = {"bound": "alu", "achieved": d_entry["Gnormal/s"], "peak": round(peak_gn, 1), "unit": "Gnormal/s",
+                "frac": round(d_entry["Gnormal/s"] / peak_gn, 4), "traffic": None,
+                "kernel": dominant, "valu_insts_per_normal": VALU_INSTS_PER_NORMAL}
+    roof.setdefault("kernel", dominant)
+    line = {
+        "metric": METRIC,
+        "value": round(W.d / (ms_step * 1e-3), 1),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{W.name}: {W.description}", "d": W.d, "K": W.K, "members": W.n,
+                   "active_subspaces": len(W.active), "weights": "bf16" if W.dtype == S.BF16 else "f32",
+                   "noise": "Philox4x32-10 + fp64 Box-Muller, fp32 FMA"},
+        "roofline": roof,
+        "ops": ops,
+    }
+    if part_ms is not None:
+        line["partition_ms"] = round(part_ms, 3)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(W, args.cpu_positions)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -16,7 +16,8 @@ namespace cpes {
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
 // 32x32->64 multiplies and xors, the key advancing by Weyl constants between
 // rounds.  The key words come from kernel arguments, so the key schedule runs
-// on the scalar unit.
+// on the scalar unit; each three-way xor is one v_bitop3_b32 (truth table
+// 0x96) on gfx950.
 
 constexpr uint32_t kPhiloxMulA = 0xD2511F53u;
 constexpr uint32_t kPhiloxMulB = 0xCD9E8D57u;
@@ -27,6 +28,11 @@ struct Words4 {
     uint32_t x, y, z, w;
 };
 
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c)
+{
+    return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
 __device__ __forceinline__ Words4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
                                                 uint32_t k0, uint32_t k1)
 {
@@ -34,8 +40,8 @@ __device__ __forceinline__ Words4 philox4x32_10(uint32_t c0, uint32_t c1, uint32
     for (int r = 0; r < 10; ++r) {
         const uint64_t pa = (uint64_t)kPhiloxMulA * c0;
         const uint64_t pb = (uint64_t)kPhiloxMulB * c2;
-        const uint32_t n0 = (uint32_t)(pb >> 32) ^ c1 ^ k0;
-        const uint32_t n2 = (uint32_t)(pa >> 32) ^ c3 ^ k1;
+        const uint32_t n0 = xor3((uint32_t)(pb >> 32), c1, k0);
+        const uint32_t n2 = xor3((uint32_t)(pa >> 32), c3, k1);
         c1 = (uint32_t)pb;
         c3 = (uint32_t)pa;
         c0 = n0;
@@ -55,89 +61,125 @@ __device__ __forceinline__ Words4 stream_block(uint32_t k0, uint32_t k1, uint32_
 // ------------------------------------------------------------ Box-Muller --
 // A pair of words (a, b) gives two normals rho cos(theta), rho sin(theta) with
 // rho = sqrt(-2 ln U(a)), theta = 2 pi U(b), U(x) = ((x >> 8) + 1) 2^-24.
-// Both factors are evaluated in fp64 (full rate on CDNA4) to ~2^-44 relative
+// Both factors are evaluated in fp64 (full rate on CDNA4) to ~2^-41 relative
 // error and their product is rounded once to fp32, so the result is the
-// correctly rounded normal except within ~2^-20 of a rounding boundary.
+// correctly rounded normal except within ~2^-17 relative of a rounding
+// boundary (and always within one fp32 ulp of it).
+//
+// Polynomial coefficients are near-minimax fits (relative error) computed
+// offline with 120-bit arithmetic; the error of each evaluation is stated.
 
-// ln U for U = m 2^-24, m in [1, 2^24]: m = f 2^e with f in (1/sqrt2, sqrt2],
-// ln U = (e - 24) ln 2 + 2 atanh((f - 1) / (f + 1)), the series truncated
-// after s^15 (relative error < 4e-14 for |s| <= 3 - 2 sqrt2).
-__device__ __forceinline__ double bm_radius(uint32_t a)
+// L = -2 ln U for U = m 2^-24, m in [1, 2^24].  m = f 2^e with f in
+// [1/sqrt2, sqrt2), ln U = (e - 24) ln 2 + 2 atanh(s), s = (f - 1) / (f + 1),
+// |s| <= 3 - 2 sqrt2; 2 atanh(s) / s is a degree-5 polynomial in s^2
+// (relative error 2^-45).  The reciprocal is the hardware estimate (2^-24)
+// refined by one Newton step.
+__device__ __forceinline__ double bm_log_term(uint32_t a)
 {
     const uint32_t m = (a >> 8) + 1u;
-    const int lz = __clz((int)m);                 // m >= 1, so lz <= 31
-    const uint32_t nm = m << lz;                  // top bit set: m = nm 2^-(lz)
-    const int big = nm > 3037000499u ? 1 : 0;     // nm 2^-31 > sqrt(2)
-    const int e = 31 - lz + big;                  // m = f 2^e
-    const double f = __builtin_ldexp((double)nm, -31 - big);
-    const double num = f - 1.0;                   // exact
-    const double den = f + 1.0;                   // exact
-    double r = __builtin_amdgcn_rcp(den);         // reciprocal estimate, refined twice
-    double err = __builtin_fma(-den, r, 1.0);
-    r = __builtin_fma(r, err, r);
-    err = __builtin_fma(-den, r, 1.0);
-    r = __builtin_fma(r, err, r);
+    int ex;
+    const double mant = __builtin_frexp((double)m, &ex);    // (double)m = mant 2^ex, mant in [1/2, 1)
+    const int low = mant < 0x1.6a09e667f3bcdp-1 ? 1 : 0;    // below 1/sqrt2: use 2 mant
+    const double f = __builtin_ldexp(mant, low);
+    const double e = (double)(ex - low - 24);
+    const double num = f - 1.0;                              // exact
+    const double den = f + 1.0;                              // exact
+    double r = __builtin_amdgcn_rcp(den);
+    r = __builtin_fma(r, __builtin_fma(-den, r, 1.0), r);
     const double s = num * r;
     const double s2 = s * s;
-    double p = 2.0 / 15.0;
-    p = __builtin_fma(p, s2, 2.0 / 13.0);
-    p = __builtin_fma(p, s2, 2.0 / 11.0);
-    p = __builtin_fma(p, s2, 2.0 / 9.0);
-    p = __builtin_fma(p, s2, 2.0 / 7.0);
-    p = __builtin_fma(p, s2, 2.0 / 5.0);
-    p = __builtin_fma(p, s2, 2.0 / 3.0);
-    p = __builtin_fma(p, s2, 2.0);
-    const double ln_f = s * p;
-    const double ln_u = __builtin_fma((double)(e - 24), 0x1.62e42fefa39efp-1, ln_f);
-    return __builtin_sqrt(-2.0 * ln_u);
+    double p = -0x1.9198127996755p-2;
+    p = __builtin_fma(p, s2, -0x1.c6208ce741fa9p-2);
+    p = __builtin_fma(p, s2, -0x1.24943960322ecp-1);
+    p = __builtin_fma(p, s2, -0x1.99999628a623ep-1);
+    p = __builtin_fma(p, s2, -0x1.5555555672df1p+0);
+    p = __builtin_fma(p, s2, -0x1.fffffffffff10p+1);        // -4 atanh(s) / s
+    return __builtin_fma(e, -0x1.62e42fefa39efp+0, s * p);   // e (-2 ln 2) - 4 atanh(s)
 }
 
-// (cos, sin)(theta) for theta = pi m 2^-23, m = (b >> 8) + 1 in [1, 2^24].
-// Quadrant and remainder are taken from m exactly; the remainder r (in units
-// of 2^-23 half-turns) is folded to t in [0, 2^21] so that theta mod pi/2 is
-// pi t 2^-23 or pi/2 minus it, and sin / cos(pi t 2^-23) are Taylor series in
-// the integer t with coefficients (-1)^k pi^n / n! 2^(-23 n) (truncation
-// error < 3e-14 relative on [0, pi/4]).  Exact zeros stay exact.
-__device__ __forceinline__ void bm_angle(uint32_t b, double& c_out, double& s_out)
+// rho = sqrt(L): hardware reciprocal square root (2^-24) and one Goldschmidt
+// step (2^-47).  The 2^-400 bias only keeps the estimate finite at L = 0
+// (it vanishes in rounding for every L > 0), so rho(-0) = -0 like sqrt.
+__device__ __forceinline__ double bm_sqrt(double L)
+{
+    const double y = __builtin_amdgcn_rsq(L + 0x1p-400);
+    const double g = L * y;
+    const double h = 0.5 * y;
+    return __builtin_fma(g, __builtin_fma(-g, h, 0.5), g);
+}
+
+__device__ __forceinline__ double bm_radius(uint32_t a)
+{
+    return bm_sqrt(bm_log_term(a));
+}
+
+// Angle theta = pi m 2^-23, m = (b >> 8) + 1 in [1, 2^24].  Quadrant and
+// remainder come from m exactly; the remainder rem (units of 2^-23
+// half-turns) is folded to t = min(rem, 2^22 - rem) in [0, 2^21], and
+// sp = sin(pi t 2^-23) (degree-5 odd-power fit, 2^-47), cp = cos(pi t 2^-23)
+// (degree 5 in t^2 with constant 1, 2^-41.6).  sp and cp are magnitudes; the
+// caller places them by quadrant: (cos, sin) = (C, S), (-S, C), (-C, -S),
+// (S, -C), with (C, S) = (cp, sp), or (sp, cp) when folded.
+struct AngleParts {
+    double sp, cp;
+    bool take_sin;       // cos theta = +-sp (and sin theta = +-cp)
+    uint32_t neg_cos;    // sign bit (bit 31) of cos theta
+    uint32_t neg_sin;    // sign bit (bit 31) of sin theta
+};
+
+__device__ __forceinline__ AngleParts bm_angle_parts(uint32_t b)
 {
     const uint32_t m = (b >> 8) + 1u;
-    const uint32_t quadrant = (m >> 22) & 3u;
     const uint32_t rem = m & 0x3FFFFFu;
     const bool fold = rem > (1u << 21);
     const double t = (double)(fold ? (1u << 22) - rem : rem);
     const double t2 = t * t;
-    double sp = 0x1.e8f434d018d63p-311;
-    sp = __builtin_fma(sp, t2, -0x1.e3074fde8871fp-261);
-    sp = __builtin_fma(sp, t2, 0x1.50783487ee782p-211);
-    sp = __builtin_fma(sp, t2, -0x1.32d2cce62bd86p-162);
-    sp = __builtin_fma(sp, t2, 0x1.466bc6775aae2p-114);
-    sp = __builtin_fma(sp, t2, -0x1.4abbce625be53p-67);
-    sp = __builtin_fma(sp, t2, 0x1.921fb54442d18p-22);
-    sp = sp * t;                                  // sin(pi t 2^-23)
-    double cp = -0x1.b6e24f44b128fp-336;
-    cp = __builtin_fma(cp, t2, 0x1.f9d38a3763cc3p-286);
-    cp = __builtin_fma(cp, t2, -0x1.a6d1f2a204a8cp-236);
-    cp = __builtin_fma(cp, t2, 0x1.e1f506891babbp-187);
-    cp = __builtin_fma(cp, t2, -0x1.55d3c7e3cbffap-138);
-    cp = __builtin_fma(cp, t2, 0x1.03c1f081b5ac4p-90);
-    cp = __builtin_fma(cp, t2, -0x1.3bd3cc9be45dep-44);
-    cp = __builtin_fma(cp, t2, 1.0);              // cos(pi t 2^-23)
-    // Rotate by the quadrant: (c, s) = (C, S), (-S, C), (-C, -S), (S, -C) where
-    // (C, S) = (cos, sin) of the remainder, i.e. (cp, sp) or, folded, (sp, cp).
-    const bool take_sin = fold ^ ((quadrant & 1u) != 0u);
-    const double mag_c = take_sin ? sp : cp;
-    const double mag_s = take_sin ? cp : sp;
-    c_out = (quadrant == 1u || quadrant == 2u) ? -mag_c : mag_c;
-    s_out = (quadrant >= 2u) ? -mag_s : mag_s;
+    double sp = -0x1.dd4e53cfc3ebep-261;
+    sp = __builtin_fma(sp, t2, 0x1.5071bed3ae526p-211);
+    sp = __builtin_fma(sp, t2, -0x1.32d2c62989f77p-162);
+    sp = __builtin_fma(sp, t2, 0x1.466bc670fd116p-114);
+    sp = __builtin_fma(sp, t2, -0x1.4abbce62577b8p-67);
+    sp = __builtin_fma(sp, t2, 0x1.921fb54442cf8p-22);
+    sp = sp * t;
+    double cp = -0x1.a1e54d0df20f1p-236;
+    cp = __builtin_fma(cp, t2, 0x1.e1ec6573b80dcp-187);
+    cp = __builtin_fma(cp, t2, -0x1.55d3c1b49a018p-138);
+    cp = __builtin_fma(cp, t2, 0x1.03c1f07e99c51p-90);
+    cp = __builtin_fma(cp, t2, -0x1.3bd3cc9be35d0p-44);
+    cp = __builtin_fma(cp, t2, 1.0);
+    AngleParts r;
+    r.sp = sp;
+    r.cp = cp;
+    r.take_sin = fold ^ (((m >> 22) & 1u) != 0u);           // odd quadrant swaps the roles
+    r.neg_cos = ((m + (1u << 22)) << 8) & 0x80000000u;      // quadrant 1 or 2
+    r.neg_sin = (m << 8) & 0x80000000u;                     // quadrant 2 or 3
+    return r;
 }
 
+// (cos, sin)(theta) as fp64 values (test hook).
+__device__ __forceinline__ void bm_angle(uint32_t b, double& c_out, double& s_out)
+{
+    const AngleParts p = bm_angle_parts(b);
+    const double mc = p.take_sin ? p.sp : p.cp;
+    const double ms = p.take_sin ? p.cp : p.sp;
+    c_out = p.neg_cos ? -mc : mc;
+    s_out = p.neg_sin ? -ms : ms;
+}
+
+// Two normals of the pair (a, b): z_even = fp32(rho cos theta), z_odd =
+// fp32(rho sin theta).  The products are formed from the magnitudes and the
+// quadrant's swap and signs are applied to the fp32 results, which is exact
+// (negation commutes with multiplication and rounding).
 __device__ __forceinline__ void bm_pair(uint32_t a, uint32_t b, float& z_even, float& z_odd)
 {
     const double rho = bm_radius(a);
-    double c, s;
-    bm_angle(b, c, s);
-    z_even = (float)(rho * c);
-    z_odd = (float)(rho * s);
+    const AngleParts p = bm_angle_parts(b);
+    const float zc = (float)(rho * p.cp);
+    const float zs = (float)(rho * p.sp);
+    const float me = p.take_sin ? zs : zc;
+    const float mo = p.take_sin ? zc : zs;
+    z_even = __uint_as_float(__float_as_uint(me) ^ p.neg_cos);
+    z_odd = __uint_as_float(__float_as_uint(mo) ^ p.neg_sin);
 }
 
 // Four normals of block q: positions 4q .. 4q+3.
