@@ -38,6 +38,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=1)
     p.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5"])
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--kernels-once", action="store_true",
+                   help="run each kernel once on one 504,654,080-position subspace (for counter passes) and exit")
     p.add_argument("--cpu-positions", type=int, default=1 << 23,
                    help="positions per subspace sample for the oracle baseline")
     return p.parse_args()
@@ -111,8 +113,10 @@ def run_step(W, cp, torch, P, timer, offsets_cache):
         aux = P["aux"][:length]
         if W.master:
             timer.run("stage_master", lambda: cp.cpes_stage_master(P["w"], s, aux))
-        for seed, sign in zip(seeds, W.signs):
-            timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigma, seed, sign, aux=aux, aux_mode=aux_mode))
+        for m, (seed, sign) in enumerate(zip(seeds, W.signs)):
+            # the first member takes the backup of the subspace; the others perturb from it
+            mode = aux_mode if (W.master or m == 0) else cp.AUX_BACKUP
+            timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigma, seed, sign, aux=aux, aux_mode=mode))
             # (the perturbed model would be evaluated here)
             timer.run("restore", lambda: cp.cpes_restore(P["w"], s, aux=aux, aux_mode=aux_mode))
         timer.run("normalize", lambda: cp.cpes_normalize_rewards(P["rewards"][t], P["rnorm"][t], W.norm_mode))
@@ -127,7 +131,9 @@ def bytes_per_position(W, op):
     e = 2 if W.dtype == S.BF16 else 4
     ix = 8 if W.partition_mode == S.PART_PERMUTATION else 0
     if op == "perturb":
-        return (4 + e if W.master else 3 * e) + ix      # read w (or master), write w (+ snapshot)
+        # master: read master, write w; else the first member reads w and writes w and the
+        # backup, the others read the backup and write w
+        return (4 + e if W.master else (3 * e + (W.n - 1) * 2 * e) / W.n) + ix
     if op == "restore":
         return (4 + e if W.master else 2 * e) + ix
     if op == "update":
@@ -159,8 +165,9 @@ def cpu_baseline(W, positions):
         t0 = time.perf_counter()
         if W.master:
             aux[:] = O.stage_master(w, 0, n)
-        for seed, sign in zip(seeds, W.signs):
-            O.perturb(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=mode)
+        for m, (seed, sign) in enumerate(zip(seeds, W.signs)):
+            pmode = mode if (W.master or m == 0) else O.AUX_BACKUP
+            O.perturb(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=pmode)
             O.restore(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=mode)
         O.normalize(W.rewards(t), W.norm_mode)
         O.update(w, 0, n, seeds, W.signs, rn, np.float32(W.alpha), np.float32(W.sigma_k(k)), W.scale_mode,
@@ -173,6 +180,41 @@ def cpu_baseline(W, positions):
             "sample": f"first {positions} positions of subspaces {list(W.active[:2])}, all {W.n} members "
                       f"(perturb+backup, restore) + normalise + update; {t_total:.1f} s, "
                       f"extrapolated per position to the full step"}
+
+
+def kernels_once(cp, torch):
+    """One warm-up and one measured launch of every kernel on the shape of the
+    c3 layer-group subspace 4 (504,654,080 bf16 positions), plus torch's copy
+    of the same bytes as the plain-copy reference for traffic counters."""
+    import synthetic as S
+
+    W = S.workload("c3")
+    L = W.sizes()[4]
+    dev = torch.device("cuda")
+    w = S.device_weights(L + 64, S.BF16, 0)
+    snap = torch.empty(L, dtype=torch.bfloat16, device=dev)
+    master = torch.empty(L, dtype=torch.float32, device=dev)
+    r = torch.from_numpy(W.rewards(0)).to(dev)
+    rn = torch.empty_like(r)
+    s = cp.subspace(0, L)
+    sigma = W.sigma_k(4)
+    seeds64 = [m + 1 for m in range(64) for _ in (0, 1)]
+    signs64 = [1, -1] * 64
+    r128 = torch.from_numpy(S.rewards("mean_bernoulli", 128, 99)).to(dev)
+    rn128 = torch.empty_like(r128)
+    for _ in range(2):
+        cp.cpes_perturb(w, s, sigma, 3, 1, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+        cp.cpes_restore(w, s, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+        cp.cpes_normalize_rewards(r, rn, cp.NORM_Z)
+        cp.cpes_update(w, s, W.member_seeds(0), W.signs, rn, W.alpha, sigma)
+        cp.cpes_stage_master(w, s, master)
+        cp.cpes_perturb(w, s, sigma, 3, 1, aux=master, aux_mode=cp.AUX_MASTER)
+        cp.cpes_restore(w, s, aux=master, aux_mode=cp.AUX_MASTER)
+        cp.cpes_normalize_rewards(r128, rn128, cp.NORM_Z)
+        cp.cpes_update(w, s, seeds64, signs64, rn128, W.alpha, sigma, master=master)
+        snap.copy_(w[:L])
+    torch.cuda.synchronize()
+    print(json.dumps({"kernels_once": "c3 subspace 4", "positions": L}), flush=True)
 
 
 def main():
@@ -189,6 +231,9 @@ def main():
     W = S.workload(args.workload)
     cp.load()
     torch.cuda.set_device(0)
+    if args.kernels_once:
+        kernels_once(cp, torch)
+        return
     P = build_plan(W, cp, torch)
     torch.cuda.synchronize()
     cache = {}

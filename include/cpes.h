@@ -67,7 +67,7 @@ enum cpes_status {
 
 enum cpes_dtype { CPES_BF16 = 0, CPES_F32 = 1 };
 enum cpes_partition_mode { CPES_PART_CONTIGUOUS = 0, CPES_PART_PERMUTATION = 1 };
-enum cpes_aux_mode { CPES_AUX_NONE = 0, CPES_AUX_SNAPSHOT = 1, CPES_AUX_MASTER = 2 };
+enum cpes_aux_mode { CPES_AUX_NONE = 0, CPES_AUX_SNAPSHOT = 1, CPES_AUX_MASTER = 2, CPES_AUX_BACKUP = 3 };
 enum cpes_norm_mode { CPES_NORM_Z = 0, CPES_NORM_RANK = 1 };
 enum cpes_scale_mode { CPES_SCALE_ALPHA_OVER_N_SIGMA = 0, CPES_SCALE_ALPHA_OVER_N = 1 };
 
@@ -129,6 +129,12 @@ CPES_API size_t cpes_partition_workspace_bytes(int mode, int64_t d, int32_t K);
  *                               before the change: the weight backup.
  *   aux_mode CPES_AUX_MASTER:   src_j = ((const float*)aux)[j], an fp32 master
  *                               of the subspace (CPES_BF16 weights only).
+ *   aux_mode CPES_AUX_BACKUP:   src_j = aux[j], an existing backup (dtype of w)
+ *                               of the unperturbed subspace, read only; w is
+ *                               not read.  Equal to restoring from the backup
+ *                               and then perturbing, in one pass.  Every member
+ *                               of a step perturbs the same pre-update weights,
+ *                               so one backup serves all of them.
  * Parameters outside the subspace are not touched.
  * Errors: w NULL, s NULL, length < 0, contiguous range beyond numel, dtype /
  *   aux_mode unknown, aux NULL when needed, sign not +-1, sigma negative or

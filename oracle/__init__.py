@@ -21,7 +21,7 @@ _SRC = os.path.join(_HERE, "cpes_oracle.c")
 _LIB = os.path.join(_HERE, "libcpes_oracle.so")
 
 BF16, F32 = 0, 1
-AUX_NONE, AUX_SNAPSHOT, AUX_MASTER = 0, 1, 2
+AUX_NONE, AUX_SNAPSHOT, AUX_MASTER, AUX_BACKUP = 0, 1, 2, 3
 NORM_Z, NORM_RANK = 0, 1
 SCALE_ALPHA_OVER_N_SIGMA, SCALE_ALPHA_OVER_N = 0, 1
 PART_CONTIGUOUS, PART_PERMUTATION = 0, 1

@@ -229,12 +229,20 @@ static int64_t param_index(const int64_t* index, int64_t offset, int64_t j)
 /* aux_mode SNAPSHOT: snap[j] receives the pre-perturbation value (the weight  */
 /*   backup of Sec. 3.3 / Supp. A.8, "CPU Weight Backup").                     */
 /* aux_mode MASTER: the source value is the fp32 master[j] instead of w.       */
+/* aux_mode BACKUP: w is first restored from an existing backup aux[j] (dtype  */
+/*   of w), then perturbed: one backup of the pre-update weights serves every  */
+/*   member of a step.                                                         */
 /* ------------------------------------------------------------------------- */
 
 int orc_perturb(void* w, int dtype, int64_t offset, int64_t length, const int64_t* index,
                 int64_t j0, float sigma, uint64_t seed, int sign, void* aux, int aux_mode)
 {
     if (sign != 1 && sign != -1) return ORC_ERR;
+    if (aux_mode == ORC_AUX_BACKUP) {
+        if (orc_restore(w, dtype, offset, length, index, j0, sigma, seed, sign, aux, ORC_AUX_SNAPSHOT) != ORC_OK)
+            return ORC_ERR;
+        return orc_perturb(w, dtype, offset, length, index, j0, sigma, seed, sign, NULL, ORC_AUX_NONE);
+    }
     float scale = (float)sign * sigma; /* exact: a sign flip */
     int64_t j;
 #pragma omp parallel for schedule(static)

@@ -18,6 +18,7 @@
 #define ORC_AUX_NONE 0
 #define ORC_AUX_SNAPSHOT 1
 #define ORC_AUX_MASTER 2
+#define ORC_AUX_BACKUP 3
 
 #define ORC_NORM_Z 0
 #define ORC_NORM_RANK 1

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(PKG, "libcpes.so")
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 BF16, F32 = 0, 1
 PART_CONTIGUOUS, PART_PERMUTATION = 0, 1
-AUX_NONE, AUX_SNAPSHOT, AUX_MASTER = 0, 1, 2
+AUX_NONE, AUX_SNAPSHOT, AUX_MASTER, AUX_BACKUP = 0, 1, 2, 3
 NORM_Z, NORM_RANK = 0, 1
 SCALE_ALPHA_OVER_N_SIGMA, SCALE_ALPHA_OVER_N = 0, 1
 MAX_MEMBERS, MAX_REWARDS, MAX_GROUPS, MAX_PERMUTATION_K = 256, 4096, 1024, 256

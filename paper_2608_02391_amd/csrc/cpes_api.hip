@@ -218,7 +218,8 @@ int cpes_perturb(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, 
     int rc = check_subspace(w_dev, numel, dtype, s, fn);
     if (rc) return rc;
     if ((rc = check_sign(sign, fn)) || (rc = check_sigma(sigma, fn))) return rc;
-    if (aux_mode != CPES_AUX_NONE && aux_mode != CPES_AUX_SNAPSHOT && aux_mode != CPES_AUX_MASTER)
+    if (aux_mode != CPES_AUX_NONE && aux_mode != CPES_AUX_SNAPSHOT && aux_mode != CPES_AUX_MASTER &&
+        aux_mode != CPES_AUX_BACKUP)
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown aux_mode %d", fn, aux_mode);
     if (aux_mode != CPES_AUX_NONE && !aux_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: aux buffer is null", fn);
     if (aux_mode == CPES_AUX_MASTER && dtype != CPES_BF16)

@@ -92,71 +92,95 @@ __device__ __forceinline__ bool param_of(const StreamArgs& a, int64_t j, int64_t
     return i >= 0 && i < a.numel;
 }
 
+// Drive a streaming kernel: every full unit goes through `vec_body` (16-byte
+// accesses; only when the subspace's vectors are aligned) or `scalar_body`
+// (element accesses) in a branch-free grid-stride loop, so that per-launch
+// invariants (polynomial constants, key schedule) stay hoisted; the ragged
+// last unit, if any, is done once by thread 0 with `scalar_body`.
+template <int N, bool VEC, typename VecBody, typename ScalarBody>
+__device__ __forceinline__ void for_each_unit(int64_t length, VecBody&& vec_body, ScalarBody&& scalar_body)
+{
+    const int64_t full = length / N;
+    if (VEC) {
+        for (int64_t u = global_tid(); u < full; u += grid_stride()) vec_body(u);
+    } else {
+        for (int64_t u = global_tid(); u < full; u += grid_stride()) scalar_body(u);
+    }
+    if (full * N < length && global_tid() == 0) scalar_body(full);
+}
+
 // ---------------------------------------------------------------- perturb --
 // w[p(j)] = cast(fmaf(scale, eps_j, src_j)); src = w (optionally backed up to
-// the snapshot first) or the fp32 master.  Also serves replay restore with
-// scale = -sign * sigma.
+// the snapshot first), the fp32 master, or an existing backup.  Also serves
+// replay restore with scale = -sign * sigma.
 template <typename T, int AUX, bool GATHER, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
 {
     constexpr int N = UnitOf<T>::n;
     T* w = static_cast<T*>(a.w);
-    const int64_t units = (a.length + N - 1) / N;
-    for (int64_t u = global_tid(); u < units; u += grid_stride()) {
+    auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
-        if (VEC && j0 + N <= a.length) {
-            float src[N];
-            T old[N];
-            int64_t idx[N];
-            if (GATHER) {
-                load_index<N>(a.index + a.offset + j0, idx);
-#pragma unroll
-                for (int e = 0; e < N; ++e) {
-                    const bool ok = idx[e] >= 0 && idx[e] < a.numel;
-                    old[e] = ok ? w[idx[e]] : T(0);
-                }
-            } else {
-                load_vec<T>(w + a.offset + j0, old);
-            }
-            if (AUX == kAuxMaster) {
-                load_f32s<N>(static_cast<const float*>(a.aux) + j0, src);
-            } else {
-#pragma unroll
-                for (int e = 0; e < N; ++e) src[e] = to_f32<T>(old[e]);
-                if (AUX == kAuxSnapshot) store_vec<T>(static_cast<T*>(a.aux) + j0, old);
-            }
-            float z[N];
-            unit_normals<N>(a.k0, a.k1, (uint64_t)j0 >> 2, z);
-            T out[N];
-#pragma unroll
-            for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src[e]));
-            if (GATHER) {
-#pragma unroll
-                for (int e = 0; e < N; ++e)
-                    if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = out[e];
-            } else {
-                store_vec<T>(w + a.offset + j0, out);
-            }
-        } else {
-            float z[N];
-            unit_normals<N>(a.k0, a.k1, (uint64_t)j0 >> 2, z);
+        float src[N];
+        T old[N];
+        int64_t idx[N];
+        if (GATHER) {
+            load_index<N>(a.index + a.offset + j0, idx);
 #pragma unroll
             for (int e = 0; e < N; ++e) {
-                const int64_t j = j0 + e;
-                int64_t i;
-                if (j >= a.length || !param_of<GATHER>(a, j, i)) continue;
-                float src;
-                if (AUX == kAuxMaster) {
-                    src = static_cast<const float*>(a.aux)[j];
-                } else {
-                    const T old = w[i];
-                    if (AUX == kAuxSnapshot) static_cast<T*>(a.aux)[j] = old;
-                    src = to_f32<T>(old);
-                }
-                w[i] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src));
+                const bool ok = idx[e] >= 0 && idx[e] < a.numel;
+                old[e] = ok ? w[idx[e]] : T(0);
             }
+        } else if (AUX != kAuxMaster && AUX != kAuxBackup) {
+            load_vec<T>(w + a.offset + j0, old);
         }
-    }
+        if (AUX == kAuxMaster) {
+            load_f32s<N>(static_cast<const float*>(a.aux) + j0, src);
+        } else if (AUX == kAuxBackup) {
+            T b[N];
+            load_vec<T>(static_cast<const T*>(a.aux) + j0, b);
+#pragma unroll
+            for (int e = 0; e < N; ++e) src[e] = to_f32<T>(b[e]);
+        } else {
+#pragma unroll
+            for (int e = 0; e < N; ++e) src[e] = to_f32<T>(old[e]);
+            if (AUX == kAuxSnapshot) store_vec<T>(static_cast<T*>(a.aux) + j0, old);
+        }
+        float z[N];
+        unit_normals<N>(a.k0, a.k1, (uint64_t)j0 >> 2, z);
+        T out[N];
+#pragma unroll
+        for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src[e]));
+        if (GATHER) {
+#pragma unroll
+            for (int e = 0; e < N; ++e)
+                if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = out[e];
+        } else {
+            store_vec<T>(w + a.offset + j0, out);
+        }
+    };
+    auto scalar_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+        float z[N];
+        unit_normals<N>(a.k0, a.k1, (uint64_t)j0 >> 2, z);
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+            const int64_t j = j0 + e;
+            int64_t i;
+            if (j >= a.length || !param_of<GATHER>(a, j, i)) continue;
+            float src;
+            if (AUX == kAuxMaster) {
+                src = static_cast<const float*>(a.aux)[j];
+            } else if (AUX == kAuxBackup) {
+                src = to_f32<T>(static_cast<const T*>(a.aux)[j]);
+            } else {
+                const T old = w[i];
+                if (AUX == kAuxSnapshot) static_cast<T*>(a.aux)[j] = old;
+                src = to_f32<T>(old);
+            }
+            w[i] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src));
+        }
+    };
+    for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
 
 // --------------------------------------------------------------- restores --
@@ -167,30 +191,30 @@ __global__ __launch_bounds__(kBlock) void k_restore_copy(StreamArgs a)
     constexpr int N = UnitOf<T>::n;
     T* w = static_cast<T*>(a.w);
     const T* snap = static_cast<const T*>(a.aux);
-    const int64_t units = (a.length + N - 1) / N;
-    for (int64_t u = global_tid(); u < units; u += grid_stride()) {
+    auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
-        if (VEC && j0 + N <= a.length) {
-            T v[N];
-            load_vec<T>(snap + j0, v);
-            if (GATHER) {
-                int64_t idx[N];
-                load_index<N>(a.index + a.offset + j0, idx);
+        T v[N];
+        load_vec<T>(snap + j0, v);
+        if (GATHER) {
+            int64_t idx[N];
+            load_index<N>(a.index + a.offset + j0, idx);
 #pragma unroll
-                for (int e = 0; e < N; ++e)
-                    if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = v[e];
-            } else {
-                store_vec<T>(w + a.offset + j0, v);
-            }
+            for (int e = 0; e < N; ++e)
+                if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = v[e];
         } else {
-#pragma unroll
-            for (int e = 0; e < N; ++e) {
-                const int64_t j = j0 + e;
-                int64_t i;
-                if (j < a.length && param_of<GATHER>(a, j, i)) w[i] = snap[j];
-            }
+            store_vec<T>(w + a.offset + j0, v);
         }
-    }
+    };
+    auto scalar_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+            const int64_t j = j0 + e;
+            int64_t i;
+            if (j < a.length && param_of<GATHER>(a, j, i)) w[i] = snap[j];
+        }
+    };
+    for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
 
 // Master restore (bf16 weights): w[p(j)] = rne_bf16(master[j]).
@@ -200,33 +224,33 @@ __global__ __launch_bounds__(kBlock) void k_restore_master(StreamArgs a)
     constexpr int N = 8;
     uint16_t* w = static_cast<uint16_t*>(a.w);
     const float* master = static_cast<const float*>(a.aux);
-    const int64_t units = (a.length + N - 1) / N;
-    for (int64_t u = global_tid(); u < units; u += grid_stride()) {
+    auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
-        if (VEC && j0 + N <= a.length) {
-            float m[N];
-            load_f32s<N>(master + j0, m);
-            uint16_t v[N];
+        float m[N];
+        load_f32s<N>(master + j0, m);
+        uint16_t v[N];
 #pragma unroll
-            for (int e = 0; e < N; ++e) v[e] = f32_to_bf16(m[e]);
-            if (GATHER) {
-                int64_t idx[N];
-                load_index<N>(a.index + a.offset + j0, idx);
+        for (int e = 0; e < N; ++e) v[e] = f32_to_bf16(m[e]);
+        if (GATHER) {
+            int64_t idx[N];
+            load_index<N>(a.index + a.offset + j0, idx);
 #pragma unroll
-                for (int e = 0; e < N; ++e)
-                    if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = v[e];
-            } else {
-                store_vec<uint16_t>(w + a.offset + j0, v);
-            }
+            for (int e = 0; e < N; ++e)
+                if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = v[e];
         } else {
-#pragma unroll
-            for (int e = 0; e < N; ++e) {
-                const int64_t j = j0 + e;
-                int64_t i;
-                if (j < a.length && param_of<GATHER>(a, j, i)) w[i] = f32_to_bf16(master[j]);
-            }
+            store_vec<uint16_t>(w + a.offset + j0, v);
         }
-    }
+    };
+    auto scalar_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+            const int64_t j = j0 + e;
+            int64_t i;
+            if (j < a.length && param_of<GATHER>(a, j, i)) w[i] = f32_to_bf16(master[j]);
+        }
+    };
+    for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
 
 // Master staging: master[j] = f32(w[p(j)]).
@@ -236,32 +260,32 @@ __global__ __launch_bounds__(kBlock) void k_stage_master(StreamArgs a)
     constexpr int N = UnitOf<T>::n;
     const T* w = static_cast<const T*>(a.w);
     float* master = static_cast<float*>(a.aux);
-    const int64_t units = (a.length + N - 1) / N;
-    for (int64_t u = global_tid(); u < units; u += grid_stride()) {
+    auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
-        if (VEC && j0 + N <= a.length) {
-            T v[N];
-            if (GATHER) {
-                int64_t idx[N];
-                load_index<N>(a.index + a.offset + j0, idx);
+        T v[N];
+        if (GATHER) {
+            int64_t idx[N];
+            load_index<N>(a.index + a.offset + j0, idx);
 #pragma unroll
-                for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
-            } else {
-                load_vec<T>(w + a.offset + j0, v);
-            }
-            float m[N];
-#pragma unroll
-            for (int e = 0; e < N; ++e) m[e] = to_f32<T>(v[e]);
-            store_f32s<N>(master + j0, m);
+            for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
         } else {
-#pragma unroll
-            for (int e = 0; e < N; ++e) {
-                const int64_t j = j0 + e;
-                int64_t i;
-                if (j < a.length && param_of<GATHER>(a, j, i)) master[j] = to_f32<T>(w[i]);
-            }
+            load_vec<T>(w + a.offset + j0, v);
         }
-    }
+        float m[N];
+#pragma unroll
+        for (int e = 0; e < N; ++e) m[e] = to_f32<T>(v[e]);
+        store_f32s<N>(master + j0, m);
+    };
+    auto scalar_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+            const int64_t j = j0 + e;
+            int64_t i;
+            if (j < a.length && param_of<GATHER>(a, j, i)) master[j] = to_f32<T>(w[i]);
+        }
+    };
+    for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
 
 // ----------------------------------------------------------------- update --
@@ -287,11 +311,7 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
     sa.index = a.index;
     sa.offset = a.offset;
     sa.numel = a.numel;
-    const int64_t units = (a.length + N - 1) / N;
-    for (int64_t u = global_tid(); u < units; u += grid_stride()) {
-        const int64_t j0 = u * N;
-        const bool full = VEC && j0 + N <= a.length;
-        float acc[N];
+    auto accumulate = [&](int64_t j0, float acc[N]) {
 #pragma unroll
         for (int e = 0; e < N; ++e) acc[e] = 0.0f;
         for (int s = 0; s < a.n_streams; ++s) {
@@ -301,53 +321,61 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
 #pragma unroll
             for (int e = 0; e < N; ++e) acc[e] = __builtin_fmaf(c, z[e], acc[e]);
         }
-        if (full) {
-            int64_t idx[N];
-            T v[N];
-            if (GATHER) {
-                load_index<N>(a.index + a.offset + j0, idx);
+    };
+    auto vec_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+        float acc[N];
+        accumulate(j0, acc);
+        int64_t idx[N];
+        T v[N];
+        if (GATHER) {
+            load_index<N>(a.index + a.offset + j0, idx);
 #pragma unroll
-                for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
-            } else if (!MASTER) {
-                load_vec<T>(w + a.offset + j0, v);
-            }
-            T out[N];
-            if (MASTER) {
-                float m[N];
-                load_f32s<N>(a.master + j0, m);
-#pragma unroll
-                for (int e = 0; e < N; ++e) {
-                    m[e] = __builtin_fmaf(a.step, acc[e], m[e]);
-                    out[e] = from_f32<T>(m[e]);
-                }
-                store_f32s<N>(a.master + j0, m);
-            } else {
-#pragma unroll
-                for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.step, acc[e], to_f32<T>(v[e])));
-            }
-            if (GATHER) {
-#pragma unroll
-                for (int e = 0; e < N; ++e)
-                    if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = out[e];
-            } else {
-                store_vec<T>(w + a.offset + j0, out);
-            }
-        } else {
+            for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
+        } else if (!MASTER) {
+            load_vec<T>(w + a.offset + j0, v);
+        }
+        T out[N];
+        if (MASTER) {
+            float m[N];
+            load_f32s<N>(a.master + j0, m);
 #pragma unroll
             for (int e = 0; e < N; ++e) {
-                const int64_t j = j0 + e;
-                int64_t i;
-                if (j >= a.length || !param_of<GATHER>(sa, j, i)) continue;
-                if (MASTER) {
-                    const float m = __builtin_fmaf(a.step, acc[e], a.master[j]);
-                    a.master[j] = m;
-                    w[i] = from_f32<T>(m);
-                } else {
-                    w[i] = from_f32<T>(__builtin_fmaf(a.step, acc[e], to_f32<T>(w[i])));
-                }
+                m[e] = __builtin_fmaf(a.step, acc[e], m[e]);
+                out[e] = from_f32<T>(m[e]);
+            }
+            store_f32s<N>(a.master + j0, m);
+        } else {
+#pragma unroll
+            for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.step, acc[e], to_f32<T>(v[e])));
+        }
+        if (GATHER) {
+#pragma unroll
+            for (int e = 0; e < N; ++e)
+                if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = out[e];
+        } else {
+            store_vec<T>(w + a.offset + j0, out);
+        }
+    };
+    auto scalar_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+        float acc[N];
+        accumulate(j0, acc);
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+            const int64_t j = j0 + e;
+            int64_t i;
+            if (j >= a.length || !param_of<GATHER>(sa, j, i)) continue;
+            if (MASTER) {
+                const float m = __builtin_fmaf(a.step, acc[e], a.master[j]);
+                a.master[j] = m;
+                w[i] = from_f32<T>(m);
+            } else {
+                w[i] = from_f32<T>(__builtin_fmaf(a.step, acc[e], to_f32<T>(w[i])));
             }
         }
-    }
+    };
+    for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
 
 // -------------------------------------------------------------- normalise --
@@ -717,9 +745,11 @@ hipError_t launch_perturb(int dtype, int aux, bool gather, bool vec, const Strea
     if (dtype == 0) {
         if (aux == kAuxSnapshot) return perturb_t<uint16_t, kAuxSnapshot>(gather, vec, a, s);
         if (aux == kAuxMaster) return perturb_t<uint16_t, kAuxMaster>(gather, vec, a, s);
+        if (aux == kAuxBackup) return perturb_t<uint16_t, kAuxBackup>(gather, vec, a, s);
         return perturb_t<uint16_t, kAuxNone>(gather, vec, a, s);
     }
     if (aux == kAuxSnapshot) return perturb_t<float, kAuxSnapshot>(gather, vec, a, s);
+    if (aux == kAuxBackup) return perturb_t<float, kAuxBackup>(gather, vec, a, s);
     return perturb_t<float, kAuxNone>(gather, vec, a, s);
 }
 

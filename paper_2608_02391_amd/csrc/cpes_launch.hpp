@@ -23,7 +23,7 @@ struct StreamArgs {
     float scale;            // +-sigma applied to the noise
 };
 
-enum AuxKind { kAuxNone = 0, kAuxSnapshot = 1, kAuxMaster = 2 };
+enum AuxKind { kAuxNone = 0, kAuxSnapshot = 1, kAuxMaster = 2, kAuxBackup = 3 };
 
 // Update: up to kMaxMembers members folded into up to kMaxMembers distinct
 // noise streams; all of it travels in the kernel argument block.

@@ -130,7 +130,8 @@ def _setup(orc, T, dtype, layout, length, wseed):
 
 @pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("length", LENGTHS)
-@pytest.mark.parametrize("dtype,aux", [(S.BF16, 0), (S.BF16, 1), (S.BF16, 2), (S.F32, 0), (S.F32, 1)])
+@pytest.mark.parametrize("dtype,aux", [(S.BF16, 0), (S.BF16, 1), (S.BF16, 2), (S.BF16, 3), (S.F32, 0), (S.F32, 1),
+                                       (S.F32, 3)])
 def test_perturb_matches_oracle(orc, T, dtype, aux, layout, length):
     w, dw, off, index, dindex = _setup(orc, T, dtype, layout, length, 1000 + length)
     sigma, seed, sign = np.float32(2.8284e-3), 17 + length, (-1 if length % 2 else 1)
@@ -141,6 +142,9 @@ def test_perturb_matches_oracle(orc, T, dtype, aux, layout, length):
         snap_d = to_dev(snap_h)
     if aux == 2:
         master_h = S.host_weights(length, S.F32, 7 + length)
+        master_d = to_dev(master_h)
+    if aux == 3:                                                      # an existing backup (other values)
+        master_h = S.host_weights(length, dtype, 9 + length)
         master_d = to_dev(master_h)
     s = cp.subspace(off, length, dindex)
     cp.cpes_perturb(dw, s, float(sigma), seed, sign, aux=snap_d if aux == 1 else master_d, aux_mode=aux)

@@ -147,6 +147,23 @@ def test_master_perturb_and_restore(orc):
     assert np.array_equal(w, w0)
 
 
+@pytest.mark.parametrize("dtype", [S.F32, S.BF16])
+def test_perturb_from_backup_is_restore_then_perturb(orc, dtype):
+    """One backup of the pre-update weights serves every member (Sec. 3.3):
+    perturbing from the backup equals restoring from it and perturbing."""
+    n, off = 5000, 40
+    w = S.host_weights(n + 100, dtype, 12)
+    backup = w[off:off + n].copy()
+    orc.perturb(w, off, n, f32(3e-3), 5, 1)                         # member 1 perturbed, not restored
+    a = w.copy()
+    orc.perturb(a, off, n, f32(3e-3), 6, -1, aux=backup, aux_mode=orc.AUX_BACKUP)
+    b = w.copy()
+    b[off:off + n] = backup
+    orc.perturb(b, off, n, f32(3e-3), 6, -1)
+    assert np.array_equal(a, b)
+    assert np.array_equal(backup, S.host_weights(n + 100, dtype, 12)[off:off + n])  # the backup is read only
+
+
 def test_replay_restore_is_not_an_identity_but_is_bounded(orc):
     """Sec. 3.3 keeps a backup because (w + d) - d != w in floating point.
     reading A10: replay restore errs by at most one fp32 ulp of max(|w|, |w'|)."""
