@@ -26,9 +26,20 @@ sys.path.insert(0, ROOT)
 METRIC = "GB/s and % HBM peak for perturb/restore + ES update (params/s) at 4B params"
 HBM_PEAK_GBPS = 8000.0                 # MI355X HBM3E
 VALU_LANE_OPS_PEAK = 256 * 64 * 2.4e9  # 256 CUs x 64 lanes x 2.4 GHz: one VALU lane-op per lane per clock
-# VALU instructions per normal of the perturb kernel (SQ_INSTS_VALU per
-# dispatch / normals per dispatch, bf16 with snapshot; see profiles/).
-VALU_INSTS_PER_NORMAL = 66.0
+# Per-kernel figures measured with rocprofv3 on a 504,654,080-position bf16
+# subspace (profiles/c3_subspace_counters.md): VALU instructions per generated
+# normal (SQ_INSTS_VALU / SQ_WAVES / normals per lane) and HBM bytes per
+# position (FETCH_SIZE x 2.0 and WRITE_SIZE x 1.0, the factors a plain copy of
+# known size reads).  Valid for the kernels as profiled; re-measure after a
+# kernel change.
+MEASURED = {
+    "perturb": {"valu_per_normal": 46.4, "hbm_bytes_first": 6.0, "hbm_bytes_rest": 4.0},
+    "perturb_master": {"valu_per_normal": 44.9, "hbm_bytes": 6.0},
+    "update": {"valu_per_normal": 41.3, "hbm_bytes": 4.0},
+    "update_master": {"valu_per_normal": 41.2, "hbm_bytes": 10.0},
+    "restore": {"hbm_bytes": 4.0},
+    "restore_master": {"hbm_bytes": 6.0},
+}
 
 
 def parse():
@@ -40,8 +51,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--kernels-once", action="store_true",
                    help="run each kernel once on one 504,654,080-position subspace (for counter passes) and exit")
-    p.add_argument("--cpu-positions", type=int, default=1 << 23,
-                   help="positions per subspace sample for the oracle baseline")
+    p.add_argument("--cpu-positions", type=int, default=None,
+                   help="positions per subspace sample for the oracle baseline (default: 2^31 / members, "
+                        "about 10-30 s of host work)")
     return p.parse_args()
 
 
@@ -205,6 +217,8 @@ def kernels_once(cp, torch):
     for _ in range(2):
         cp.cpes_perturb(w, s, sigma, 3, 1, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
         cp.cpes_restore(w, s, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+        cp.cpes_perturb(w, s, sigma, 4, -1, aux=snap, aux_mode=cp.AUX_BACKUP)
+        cp.cpes_restore(w, s, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
         cp.cpes_normalize_rewards(r, rn, cp.NORM_Z)
         cp.cpes_update(w, s, W.member_seeds(0), W.signs, rn, W.alpha, sigma)
         cp.cpes_stage_master(w, s, master)
@@ -282,15 +296,25 @@ def main():
         ops[op] = entry
     dominant = max((o for o in ops if o != "normalize"), key=lambda o: ops[o]["ms_per_step"])
     d_entry = ops[dominant]
-    if dominant == "restore" or dominant == "stage_master":
+    gather = W.partition_mode == S.PART_PERMUTATION
+    key = dominant + ("_master" if W.master and dominant in ("perturb", "update", "restore") else "")
+    meas = None if (gather or W.dtype != S.BF16) else MEASURED.get(key)
+    traffic = None
+    if meas is not None:
+        per_pos = meas.get("hbm_bytes")
+        if per_pos is None:                          # first member takes the backup, the rest read it
+            per_pos = (meas["hbm_bytes_first"] + (W.n - 1) * meas["hbm_bytes_rest"]) / W.n
+        traffic = round(per_pos * d_entry["positions_per_launch"])
+    if dominant in ("restore", "stage_master"):
         roof = {"bound": "hbm", "achieved": d_entry["GB/s"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(d_entry["GB/s"] / HBM_PEAK_GBPS, 4), "traffic": None}
+                "frac": round(d_entry["GB/s"] / HBM_PEAK_GBPS, 4), "traffic": traffic, "kernel": dominant}
     else:
-        peak_gn = VALU_LANE_OPS_PEAK / VALU_INSTS_PER_NORMAL / 1e9
+        valu = (meas or {}).get("valu_per_normal", MEASURED["perturb"]["valu_per_normal"])
+        peak_gn = VALU_LANE_OPS_PEAK / valu / 1e9
         roof = {"bound": "alu", "achieved": d_entry["Gnormal/s"], "peak": round(peak_gn, 1), "unit": "Gnormal/s",
-                "frac": round(d_entry["Gnormal/s"] / peak_gn, 4), "traffic": None,
-                "kernel": dominant, "valu_insts_per_normal": VALU_INSTS_PER_NORMAL}
-    roof.setdefault("kernel", dominant)
+                "frac": round(d_entry["Gnormal/s"] / peak_gn, 4), "traffic": traffic, "kernel": dominant,
+                "valu_insts_per_normal": valu,
+                "note": "peak = VALU issue rate (256 CUs x 64 lanes x 2.4 GHz) / VALU instructions per normal"}
     line = {
         "metric": METRIC,
         "value": round(W.d / (ms_step * 1e-3), 1),
@@ -313,7 +337,8 @@ def main():
     if part_ms is not None:
         line["partition_ms"] = round(part_ms, 3)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(W, args.cpu_positions)
+        positions = args.cpu_positions or (1 << 31) // W.n
+        line["cpu_baseline"] = cpu_baseline(W, positions)
     print(json.dumps(line), flush=True)
 
 
