@@ -76,6 +76,7 @@ enum cpes_scale_mode { CPES_SCALE_ALPHA_OVER_N_SIGMA = 0, CPES_SCALE_ALPHA_OVER_
 #define CPES_MAX_REWARDS 4096        /* rewards per cpes_normalize_rewards call */
 #define CPES_MAX_GROUPS 1024         /* reward groups per cpes_normalize_rewards call */
 #define CPES_MAX_PERMUTATION_K 256   /* subspaces of a CPES_PART_PERMUTATION partition */
+#define CPES_MAX_STEP_SUBSPACES 32   /* subspaces per cpes_update_step call */
 
 typedef struct cpes_subspace {
     int64_t offset;        /* first parameter (index == NULL) or first map entry */
@@ -209,6 +210,37 @@ CPES_API int cpes_normalize_rewards(const float* r_dev, int32_t n, int mode, con
 CPES_API int cpes_update(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float* master_dev,
                 int32_t n, const uint64_t* seeds_host, const int8_t* signs_host,
                 const float* rnorm_dev, float alpha, float sigma, int scale_mode, void* stream);
+
+/*
+ * cpes_update_step -- the whole CoPES update of one step in one launch
+ * (Eq. 13; Alg. 1, after joint standardisation): for every subspace k of a
+ * partition,  theta_{S_k} += step_k * sum_{i in members of k} sign_i rnorm_i eps(seed_i),
+ *   step_k = alpha / (n_k sigma_k)  (CPES_SCALE_ALPHA_OVER_N_SIGMA) or
+ *   step_k = alpha / n_k            (CPES_SCALE_ALPHA_OVER_N; Eq. 13 with n_k = N_k),
+ * where n_k counts the members of subspace k.  With K = 1 and alpha / N this
+ * is the standard ES update of Eq. 6.  Subspaces are disjoint, so the result
+ * equals K cpes_update calls in any order.
+ * offsets_host (K+1, non-decreasing): subspace k is positions [offsets[k],
+ *   offsets[k+1]) -- parameters themselves (index_dev == NULL; offsets[K] <=
+ *   numel) or entries of the int64 device map index_dev (e.g. the output of
+ *   cpes_partition).  Noise position j is counted from offsets[k].
+ * seeds_host / signs_host / subspace_host (host, n entries): member i has seed,
+ *   sign +-1 and the subspace it perturbed; rnorm_dev (device float32[n]) its
+ *   standardised reward (joint or per group, cpes_normalize_rewards).
+ *   Members of one subspace sharing a seed share one noise stream.
+ * sigma_host (host, K): the effective sigma_k each subspace was perturbed with.
+ * Subspaces without members are left unchanged.  Each weight is read and
+ * written once; accumulation in fp32 as in cpes_update.
+ * Errors: NULL pointers, K < 1, n < 1, a sign not +-1, a member's subspace
+ *   outside [0, K), decreasing offsets, contiguous range beyond numel, alpha
+ *   not finite, sigma_k <= 0 for a subspace with members under the
+ *   OVER_N_SIGMA scale -> CPES_ERR_INVALID_ARGUMENT; K above
+ *   CPES_MAX_STEP_SUBSPACES or n above CPES_MAX_MEMBERS -> CPES_ERR_UNSUPPORTED.
+ */
+CPES_API int cpes_update_step(void* w_dev, int64_t numel, int dtype, int32_t K, const int64_t* offsets_host,
+                              const int64_t* index_dev, int32_t n, const uint64_t* seeds_host,
+                              const int8_t* signs_host, const int32_t* subspace_host, const float* rnorm_dev,
+                              float alpha, const float* sigma_host, int scale_mode, void* stream);
 
 /* ---------------- test hooks and measurement utilities ------------------ */
 

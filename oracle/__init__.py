@@ -75,6 +75,7 @@ def lib() -> ctypes.CDLL:
         L.orc_stage_master.argtypes = [vp, i32, i64, i64, vp, vp]
         L.orc_normalize.argtypes = [vp, i32, i32, vp, vp, ctypes.POINTER(ctypes.c_int)]
         L.orc_update.argtypes = [vp, i32, i64, i64, vp, i64, vp, i32, vp, vp, vp, f32, f32, i32]
+        L.orc_update_step.argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, vp, vp, f32, vp, i32]
         L.orc_prp.argtypes = [u64, i64, i64]
         L.orc_prp.restype = i64
         L.orc_bucket.argtypes = [u64, i64, ctypes.c_int32, i64]
@@ -211,6 +212,21 @@ def update(w, offset, length, seeds, signs, rnorm, alpha, sigma, scale_mode=SCAL
     _check(lib().orc_update(_ptr(w), _dtype_code(w), offset, length, _ptr(index), j0, _ptr(master),
                             seeds.size, _ptr(seeds), _ptr(signs), _ptr(rnorm), alpha, sigma,
                             scale_mode), "update")
+
+
+def update_step(w, offsets, seeds, signs, subspaces, rnorm, alpha, sigmas, scale_mode=SCALE_ALPHA_OVER_N_SIGMA,
+                index=None):
+    offsets = np.ascontiguousarray(offsets, dtype=np.int64)
+    K = offsets.size - 1
+    seeds = np.ascontiguousarray(seeds, dtype=np.uint64)
+    signs = np.ascontiguousarray(signs, dtype=np.int8)
+    subspaces = np.ascontiguousarray(subspaces, dtype=np.int32)
+    rnorm = np.ascontiguousarray(rnorm, dtype=np.float32)
+    sigmas = np.ascontiguousarray(sigmas, dtype=np.float32)
+    assert seeds.size == signs.size == subspaces.size == rnorm.size and sigmas.size == K
+    _check(lib().orc_update_step(_ptr(w), _dtype_code(w), K, _ptr(offsets), _ptr(index), seeds.size, _ptr(seeds),
+                                 _ptr(signs), _ptr(subspaces), _ptr(rnorm), alpha, _ptr(sigmas), scale_mode),
+           "update_step")
 
 
 def prp(seed: int, d: int, x: int) -> int:

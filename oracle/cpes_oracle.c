@@ -414,6 +414,33 @@ int orc_update(void* w, int dtype, int64_t offset, int64_t length, const int64_t
     return ORC_OK;
 }
 
+/* One CoPES step's update, Eq. (13) and the last loop of Alg. 1:            */
+/*   g_k = (1/N_k) sum_i rhat_{k,i} eps_{k,i};  theta+ = theta + alpha sum_k P_k g_k */
+/* (with step_k = alpha / (N_k sigma_k) under scale_mode 0).  Subspace k is    */
+/* positions [offsets[k], offsets[k+1]) of the parameters or of `index`; its  */
+/* members are those with subspace[i] == k, in order.  Supports are disjoint, */
+/* so the subspaces are updated one after the other from the same theta.     */
+int orc_update_step(void* w, int dtype, int K, const int64_t* offsets, const int64_t* index, int n,
+                    const uint64_t* seeds, const int8_t* signs, const int* subspace, const float* rnorm,
+                    float alpha, const float* sigmas, int scale_mode)
+{
+    uint64_t* ks = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)n);
+    int8_t* kg = (int8_t*)malloc((size_t)n);
+    float* kr = (float*)malloc(sizeof(float) * (size_t)n);
+    if (!ks || !kg || !kr) { free(ks); free(kg); free(kr); return ORC_ERR; }
+    int rc = ORC_OK;
+    for (int k = 0; k < K && rc == ORC_OK; ++k) {
+        int nk = 0;
+        for (int i = 0; i < n; ++i)
+            if (subspace[i] == k) { ks[nk] = seeds[i]; kg[nk] = signs[i]; kr[nk] = rnorm[i]; ++nk; }
+        if (nk == 0) continue;
+        rc = orc_update(w, dtype, offsets[k], offsets[k + 1] - offsets[k], index, 0, NULL, nk, ks, kg, kr,
+                        alpha, sigmas[k], scale_mode);
+    }
+    free(ks); free(kg); free(kr);
+    return rc;
+}
+
 /* ------------------------------------------------------------------------- */
 /* Partition of Eq. (7): disjoint subspaces covering all d indices, sizes     */
 /* d/K (within one when K does not divide d).                                  */

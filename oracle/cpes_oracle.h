@@ -56,6 +56,10 @@ int orc_update(void* w, int dtype, int64_t offset, int64_t length, const int64_t
                int64_t j0, float* master, int n, const uint64_t* seeds, const int8_t* signs,
                const float* rnorm, float alpha, float sigma, int scale_mode);
 
+int orc_update_step(void* w, int dtype, int K, const int64_t* offsets, const int64_t* index, int n,
+                    const uint64_t* seeds, const int8_t* signs, const int* subspace, const float* rnorm,
+                    float alpha, const float* sigmas, int scale_mode);
+
 int64_t orc_prp(uint64_t seed, int64_t d, int64_t x);
 int32_t orc_bucket(uint64_t seed, int64_t d, int32_t K, int64_t i);
 int orc_partition(int mode, int64_t d, int32_t K, uint64_t seed, const int64_t* bounds,

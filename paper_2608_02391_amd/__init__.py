@@ -21,11 +21,11 @@ PART_CONTIGUOUS, PART_PERMUTATION = 0, 1
 AUX_NONE, AUX_SNAPSHOT, AUX_MASTER, AUX_BACKUP = 0, 1, 2, 3
 NORM_Z, NORM_RANK = 0, 1
 SCALE_ALPHA_OVER_N_SIGMA, SCALE_ALPHA_OVER_N = 0, 1
-MAX_MEMBERS, MAX_REWARDS, MAX_GROUPS, MAX_PERMUTATION_K = 256, 4096, 1024, 256
+MAX_MEMBERS, MAX_REWARDS, MAX_GROUPS, MAX_PERMUTATION_K, MAX_STEP_SUBSPACES = 256, 4096, 1024, 256, 32
 
 EXPORTED = (
     "cpes_partition", "cpes_partition_workspace_bytes", "cpes_perturb", "cpes_restore",
-    "cpes_stage_master", "cpes_normalize_rewards", "cpes_update", "cpes_debug_philox",
+    "cpes_stage_master", "cpes_normalize_rewards", "cpes_update", "cpes_update_step", "cpes_debug_philox",
     "cpes_debug_normals", "cpes_debug_bm_grid", "cpes_debug_prp", "cpes_rng_probe",
     "cpes_last_error", "cpes_abi_version",
 )
@@ -63,6 +63,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "cpes_stage_master": [vp, i64, i32, sp, vp, vp],
         "cpes_normalize_rewards": [vp, i32, i32, vp, i32, vp, vp, vp],
         "cpes_update": [vp, i64, i32, sp, vp, i32, vp, vp, vp, f32, f32, i32, vp],
+        "cpes_update_step": [vp, i64, i32, i32, vp, vp, i32, vp, vp, vp, vp, f32, vp, i32, vp],
         "cpes_debug_philox": [u64, u32, u64, i64, vp, vp],
         "cpes_debug_normals": [u64, i64, i64, vp, vp],
         "cpes_debug_bm_grid": [u32, i64, vp, vp, vp, vp],
@@ -185,6 +186,25 @@ def cpes_update(w, s: Subspace, seeds: Sequence[int], signs: Sequence[int], rnor
     _check(load().cpes_update(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s),
                               _dev_ptr(master, "master"), n, cs, cg, _dev_ptr(rnorm, "rnorm"), alpha, sigma,
                               scale_mode, _stream(stream)))
+
+
+def cpes_update_step(w, offsets: Sequence[int], seeds: Sequence[int], signs: Sequence[int],
+                     subspaces: Sequence[int], rnorm, alpha: float, sigmas: Sequence[float],
+                     scale_mode: int = SCALE_ALPHA_OVER_N_SIGMA, index=None, stream=None) -> None:
+    """Update every subspace of a partition with its own members (one launch)."""
+    K = len(offsets) - 1
+    n = len(seeds)
+    if not (len(signs) == len(subspaces) == n) or len(sigmas) != K:
+        raise ValueError("inconsistent member or subspace arrays")
+    co = (ctypes.c_int64 * (K + 1))(*[int(x) for x in offsets])
+    cs = (ctypes.c_uint64 * n)(*[int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds])
+    cg = (ctypes.c_int8 * n)(*[int(x) for x in signs])
+    ck = (ctypes.c_int32 * n)(*[int(x) for x in subspaces])
+    csg = (ctypes.c_float * K)(*[float(x) for x in sigmas])
+    if index is not None and index.dtype != _torch().int64:
+        raise TypeError("index map must be int64")
+    _check(load().cpes_update_step(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), K, co, _dev_ptr(index, "index"), n,
+                                   cs, cg, ck, _dev_ptr(rnorm, "rnorm"), alpha, csg, scale_mode, _stream(stream)))
 
 
 def cpes_debug_philox(seed: int, domain: int, q0: int, nblocks: int, out, stream=None) -> None:

@@ -352,6 +352,91 @@ int cpes_update(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, f
     return hip_status(cpes::launch_update(dtype, master_dev != nullptr, s->index != nullptr, vec, a, (hipStream_t)stream), fn);
 }
 
+int cpes_update_step(void* w_dev, int64_t numel, int dtype, int32_t K, const int64_t* offsets_host,
+                     const int64_t* index_dev, int32_t n, const uint64_t* seeds_host, const int8_t* signs_host,
+                     const int32_t* subspace_host, const float* rnorm_dev, float alpha, const float* sigma_host,
+                     int scale_mode, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_update_step";
+    if (!w_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: weight pointer is null", fn);
+    if (dtype != CPES_BF16 && dtype != CPES_F32) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown dtype %d", fn, dtype);
+    if (K < 1) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: K %d < 1", fn, K);
+    if (K > CPES_MAX_STEP_SUBSPACES) return fail(CPES_ERR_UNSUPPORTED, "%s: K %d above CPES_MAX_STEP_SUBSPACES", fn, K);
+    if (!offsets_host || !seeds_host || !signs_host || !subspace_host || !rnorm_dev || !sigma_host)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: null offsets, members, rewards or sigmas", fn);
+    if (n < 1) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: n %d < 1", fn, n);
+    if (n > CPES_MAX_MEMBERS) return fail(CPES_ERR_UNSUPPORTED, "%s: n %d above CPES_MAX_MEMBERS", fn, n);
+    if (scale_mode != CPES_SCALE_ALPHA_OVER_N_SIGMA && scale_mode != CPES_SCALE_ALPHA_OVER_N)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown scale_mode %d", fn, scale_mode);
+    if (!std::isfinite(alpha)) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: alpha is not finite", fn);
+    if (offsets_host[0] < 0) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: offsets[0] < 0", fn);
+    for (int32_t k = 0; k < K; ++k)
+        if (offsets_host[k + 1] < offsets_host[k]) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: offsets decrease at %d", fn, k);
+    if (!index_dev && offsets_host[K] > numel)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: offsets[K] %lld exceeds numel %lld", fn, (long long)offsets_host[K],
+                    (long long)numel);
+    int count[CPES_MAX_STEP_SUBSPACES] = {0};
+    for (int32_t i = 0; i < n; ++i) {
+        int rc = check_sign(signs_host[i], fn);
+        if (rc) return rc;
+        if (subspace_host[i] < 0 || subspace_host[i] >= K)
+            return fail(CPES_ERR_INVALID_ARGUMENT, "%s: member %d names subspace %d", fn, i, subspace_host[i]);
+        ++count[subspace_host[i]];
+    }
+    cpes::StepArgs a;
+    std::memset(&a, 0, sizeof a);
+    // streams: distinct (subspace, seed) pairs, grouped by subspace, in order of first appearance
+    int n_streams = 0;
+    for (int32_t k = 0; k < K; ++k) {
+        a.stream_begin[k] = n_streams;
+        for (int32_t i = 0; i < n; ++i) {
+            if (subspace_host[i] != k) continue;
+            int u = a.stream_begin[k];
+            while (u < n_streams && ((uint64_t)a.seed_lo[u] | ((uint64_t)a.seed_hi[u] << 32)) != seeds_host[i]) ++u;
+            if (u == n_streams) {
+                a.seed_lo[u] = (uint32_t)seeds_host[i];
+                a.seed_hi[u] = (uint32_t)(seeds_host[i] >> 32);
+                ++n_streams;
+            }
+            a.member_stream[i] = (uint8_t)u;
+            a.member_sign[i] = signs_host[i];
+        }
+        if (count[k] > 0) {
+            const float sig = sigma_host[k];
+            if (scale_mode == CPES_SCALE_ALPHA_OVER_N_SIGMA && (!std::isfinite(sig) || sig <= 0.0f))
+                return fail(CPES_ERR_INVALID_ARGUMENT, "%s: sigma[%d] %g must be finite and > 0", fn, k, (double)sig);
+            const double step = scale_mode == CPES_SCALE_ALPHA_OVER_N_SIGMA
+                                    ? (double)alpha / ((double)count[k] * (double)sig)
+                                    : (double)alpha / (double)count[k];
+            a.step[k] = (float)step;
+        }
+    }
+    a.stream_begin[K] = n_streams;
+    const int N = dtype == CPES_BF16 ? 8 : 4;
+    int64_t tiles = 0;
+    for (int32_t k = 0; k <= K; ++k) {
+        a.offset[k] = offsets_host[k];
+        a.tile_begin[k] = tiles;
+        if (k == K) break;
+        const int64_t len = offsets_host[k + 1] - offsets_host[k];
+        const int64_t units = (len + N - 1) / N;
+        if (count[k] > 0) tiles += (units + 63) / 64;   // subspaces without members are left alone
+        const void* first = index_dev ? (const void*)(index_dev + offsets_host[k])
+                                      : (const void*)(static_cast<const char*>(w_dev) + (size_t)offsets_host[k] * elem_size(dtype));
+        if (aligned16(first)) a.vec_mask |= 1u << k;
+    }
+    a.w = w_dev;
+    a.index = index_dev;
+    a.rnorm = rnorm_dev;
+    a.numel = numel;
+    a.K = K;
+    a.n_members = n;
+    a.n_streams = n_streams;
+    if (tiles == 0) return CPES_OK;
+    return hip_status(cpes::launch_update_step(dtype, index_dev != nullptr, a, (hipStream_t)stream), fn);
+}
+
 int cpes_debug_philox(uint64_t seed, uint32_t domain, uint64_t q0, int64_t nblocks, uint32_t* out_dev, void* stream)
 {
     g_error.clear();

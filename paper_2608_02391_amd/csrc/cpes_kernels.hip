@@ -378,6 +378,78 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
 
+// ------------------------------------------------------------ step update --
+// theta += sum_k P_k step_k sum_{u in streams of k} c_u eps_u (Eq. 13, Alg. 1):
+// every subspace of the partition with its own members, in one launch.  Units
+// restart at each subspace's first position, so noise position j is always
+// relative to the subspace; each wave works on 64 units of one subspace.
+template <typename T, bool GATHER>
+__global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
+{
+    constexpr int N = UnitOf<T>::n;
+    __shared__ float coef[kMaxMembers];
+    for (int u = threadIdx.x; u < a.n_streams; u += blockDim.x) {
+        double c = 0.0;
+        for (int i = 0; i < a.n_members; ++i)
+            if (a.member_stream[i] == u) c += (double)a.member_sign[i] * (double)a.rnorm[i];
+        coef[u] = (float)c;
+    }
+    __syncthreads();
+    T* w = static_cast<T*>(a.w);
+    const int lane = threadIdx.x & 63;
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / 64);
+    const int64_t wave = (int64_t)blockIdx.x * (kBlock / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+    const int64_t tiles = a.tile_begin[a.K];
+    for (int64_t t = wave; t < tiles; t += waves) {
+        int k = 0;
+        while (k + 1 < a.K && a.tile_begin[k + 1] <= t) ++k;
+        const int64_t base = a.offset[k];
+        const int64_t len = a.offset[k + 1] - base;
+        const int64_t j0 = ((t - a.tile_begin[k]) * 64 + lane) * N;
+        if (j0 >= len) continue;
+        float acc[N];
+#pragma unroll
+        for (int e = 0; e < N; ++e) acc[e] = 0.0f;
+        for (int st = a.stream_begin[k]; st < a.stream_begin[k + 1]; ++st) {
+            const float c = coef[st];
+            float z[N];
+            unit_normals<N>(a.seed_lo[st], a.seed_hi[st], (uint64_t)j0 >> 2, z);
+#pragma unroll
+            for (int e = 0; e < N; ++e) acc[e] = __builtin_fmaf(c, z[e], acc[e]);
+        }
+        const float step = a.step[k];
+        if (((a.vec_mask >> k) & 1u) && j0 + N <= len) {
+            T v[N], out[N];
+            int64_t idx[N];
+            if (GATHER) {
+                load_index<N>(a.index + base + j0, idx);
+#pragma unroll
+                for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
+            } else {
+                load_vec<T>(w + base + j0, v);
+            }
+#pragma unroll
+            for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(step, acc[e], to_f32<T>(v[e])));
+            if (GATHER) {
+#pragma unroll
+                for (int e = 0; e < N; ++e)
+                    if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = out[e];
+            } else {
+                store_vec<T>(w + base + j0, out);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < N; ++e) {
+                const int64_t j = j0 + e;
+                if (j >= len) continue;
+                const int64_t i = GATHER ? a.index[base + j] : base + j;
+                if (GATHER && (i < 0 || i >= a.numel)) continue;
+                w[i] = from_f32<T>(__builtin_fmaf(step, acc[e], to_f32<T>(w[i])));
+            }
+        }
+    }
+}
+
 // -------------------------------------------------------------- normalise --
 // One workgroup.  Group statistics are summed in fp64 in index order (one
 // thread per group), exactly as the definition reads; ranks count smaller and
@@ -788,6 +860,20 @@ hipError_t launch_update(int dtype, bool master, bool gather, bool vec, const Up
 {
     if (dtype == 0) return master ? update_t<uint16_t, true>(gather, vec, a, s) : update_t<uint16_t, false>(gather, vec, a, s);
     return update_t<float, false>(gather, vec, a, s);
+}
+
+hipError_t launch_update_step(int dtype, bool gather, const StepArgs& a, hipStream_t s)
+{
+    const int64_t waves_needed = a.tile_begin[a.K];
+    const int64_t blocks = grid_for(waves_needed * 64);
+    if (dtype == 0) {
+        if (gather) hipLaunchKernelGGL((k_update_step<uint16_t, true>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a);
+        else hipLaunchKernelGGL((k_update_step<uint16_t, false>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a);
+    } else {
+        if (gather) hipLaunchKernelGGL((k_update_step<float, true>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a);
+        else hipLaunchKernelGGL((k_update_step<float, false>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a);
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_normalize(const NormalizeArgs& a, hipStream_t s)

@@ -46,6 +46,30 @@ struct UpdateArgs {
     int8_t member_sign[kMaxMembers];
 };
 
+// Whole-step update: every subspace of a partition with its own members, one
+// launch.  Waves take tiles of 64 units from a single subspace, so the
+// subspace (and its noise streams) is uniform across a wave.
+constexpr int kMaxStepSubspaces = 32;
+
+struct StepArgs {
+    void* w;
+    const int64_t* index;                          // null: contiguous
+    const float* rnorm;
+    int64_t numel;
+    int32_t K;
+    int32_t n_members;
+    int32_t n_streams;
+    uint32_t vec_mask;                             // bit k: subspace k takes 16-byte vectors
+    int64_t offset[kMaxStepSubspaces + 1];         // subspace k = positions [offset[k], offset[k+1])
+    int64_t tile_begin[kMaxStepSubspaces + 1];     // first wave tile of subspace k
+    int32_t stream_begin[kMaxStepSubspaces + 1];   // streams of subspace k
+    float step[kMaxStepSubspaces];
+    uint32_t seed_lo[kMaxMembers];
+    uint32_t seed_hi[kMaxMembers];
+    uint8_t member_stream[kMaxMembers];
+    int8_t member_sign[kMaxMembers];
+};
+
 struct NormalizeArgs {
     const float* r;
     const int32_t* group;
@@ -81,6 +105,7 @@ hipError_t launch_restore_copy(int dtype, bool gather, bool vec, const StreamArg
 hipError_t launch_restore_master(bool gather, bool vec, const StreamArgs& a, hipStream_t s);
 hipError_t launch_stage_master(int dtype, bool gather, bool vec, const StreamArgs& a, hipStream_t s);
 hipError_t launch_update(int dtype, bool master, bool gather, bool vec, const UpdateArgs& a, hipStream_t s);
+hipError_t launch_update_step(int dtype, bool gather, const StepArgs& a, hipStream_t s);
 hipError_t launch_normalize(const NormalizeArgs& a, hipStream_t s);
 hipError_t launch_partition(const PartitionArgs& a, hipStream_t s);
 hipError_t launch_debug_philox(uint64_t seed, uint32_t domain, uint64_t q0, int64_t nblocks,

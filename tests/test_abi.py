@@ -163,3 +163,26 @@ def test_binding_raises_without_fallback(tmp_path):
             mod.load(str(tmp_path / "missing.so"))
     finally:
         mod._lib = saved
+
+
+def test_update_step_rejects_bad_arguments(lib):
+    off = (ctypes.c_int64 * 3)(0, 32, 64)
+    seeds = (ctypes.c_uint64 * 4)(1, 2, 3, 4)
+    signs = (ctypes.c_int8 * 4)(1, 1, -1, 1)
+    subs = (ctypes.c_int32 * 4)(0, 0, 1, 1)
+    bad_subs = (ctypes.c_int32 * 4)(0, 0, 2, 1)
+    sig = (ctypes.c_float * 2)(2e-3, 2e-3)
+    zero_sig = (ctypes.c_float * 2)(2e-3, 0.0)
+    dec = (ctypes.c_int64 * 3)(0, 40, 32)
+    def call(**kw):
+        return lib.cpes_update_step(kw.get("w", FAKE), kw.get("numel", 64), cp.BF16, kw.get("K", 2), kw.get("off", off),
+                                    None, 4, seeds, signs, kw.get("subs", subs), FAKE, 5e-4, kw.get("sig", sig),
+                                    kw.get("scale", 0), None)
+    assert call(w=None) == cp.ERR_INVALID_ARGUMENT
+    assert call(K=0) == cp.ERR_INVALID_ARGUMENT
+    assert call(K=40) == cp.ERR_UNSUPPORTED
+    assert call(subs=bad_subs) == cp.ERR_INVALID_ARGUMENT
+    assert call(sig=zero_sig) == cp.ERR_INVALID_ARGUMENT
+    assert call(off=dec) == cp.ERR_INVALID_ARGUMENT
+    assert call(numel=63) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_last_error().decode().startswith("cpes_update_step")

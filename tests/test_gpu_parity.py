@@ -334,3 +334,68 @@ def test_prp_values_bit_exact(orc, T):
         for k in range(0, n, 37):
             assert p[k] == orc.prp(33, d, i0 + k)
             assert b[k] == orc.bucket(33, d, K, i0 + k)
+
+
+# ------------------------------------------------------------ step update --
+
+STEP_CASES = {
+    # name: (d, K, partition, members per subspace)
+    "paper_perm_k4_n40": ((1 << 20) + 3, 4, "perm", [10, 10, 10, 10]),
+    "contig_unaligned": (300007, 3, [0, 1001, 150003, 300007], [5, 3, 4]),
+    "contig_k1_std_es": (262147, 1, "equal", [8]),
+    "contig_k8_empty": ((1 << 19) + 64, 8, "equal", [2, 0, 3, 1, 1, 0, 2, 2]),
+}
+
+
+@pytest.mark.parametrize("case", list(STEP_CASES))
+@pytest.mark.parametrize("dtype", [S.BF16, S.F32])
+@pytest.mark.parametrize("scale", [S.SCALE_ALPHA_OVER_N, S.SCALE_ALPHA_OVER_N_SIGMA])
+def test_update_step_matches_oracle(orc, T, case, dtype, scale):
+    d, K, part, per = STEP_CASES[case]
+    index = dindex = None
+    if part == "perm":
+        offsets, index = orc.partition(orc.PART_PERMUTATION, d, K, seed=33)
+        dindex = to_dev(index)
+    elif part == "equal":
+        offsets, _ = orc.partition(orc.PART_CONTIGUOUS, d, K)
+    else:
+        offsets = np.array(part, dtype=np.int64)
+    offsets = [int(x) for x in offsets]
+    subs = [k for k in range(K) for _ in range(per[k])]
+    n = len(subs)
+    seeds = [1 + i for i in range(n)]
+    signs = [1 if i % 3 else -1 for i in range(n)]
+    rhat, _ = orc.normalize(S.rewards("uniform", n, 99), S.NORM_Z)        # joint standardisation (Eq. 12)
+    sigmas = [float(np.float32(1e-3 * np.sqrt(d / max(1, offsets[k + 1] - offsets[k])))) for k in range(K)]
+    w = S.host_weights(d, dtype, 70)
+    dw = to_dev(w)
+    cp.cpes_update_step(dw, offsets, seeds, signs, subs, to_dev(rhat), 5e-4, sigmas, scale, index=dindex)
+    orc.update_step(w, offsets, seeds, signs, subs, rhat, np.float32(5e-4), np.float32(sigmas), scale, index=index)
+    _sync(T)
+    got = to_host(dw)
+    if dtype == S.BF16:
+        assert bf16_close(got, w), describe_mismatch(bf16_value(got), bf16_value(w))
+    else:
+        assert f32_close(got, w), describe_mismatch(got, w)
+
+
+def test_update_step_with_grouped_standardisation(orc, T):
+    """The independent z-score ablation: each subspace standardised on its own."""
+    d, K, Nk = (1 << 18) + 5, 4, 6
+    offsets, index = orc.partition(orc.PART_PERMUTATION, d, K, seed=7)
+    subs = np.repeat(np.arange(K), Nk).astype(np.int32)
+    n = K * Nk
+    r = S.rewards("uniform", n, 5)
+    rn = T.empty(n, dtype=T.float32, device="cuda")
+    cp.cpes_normalize_rewards(to_dev(r), rn, cp.NORM_Z, group=to_dev(subs), n_groups=K)
+    rhat, _ = orc.normalize(r, S.NORM_Z, subs)
+    w = S.host_weights(d, S.BF16, 71)
+    dw = to_dev(w)
+    sig = [2e-3] * K
+    cp.cpes_update_step(dw, [int(x) for x in offsets], list(range(1, n + 1)), [1] * n, subs.tolist(), rn, 5e-4, sig,
+                        S.SCALE_ALPHA_OVER_N, index=to_dev(index))
+    orc.update_step(w, offsets, list(range(1, n + 1)), [1] * n, subs, rhat, np.float32(5e-4), np.float32(sig),
+                    S.SCALE_ALPHA_OVER_N, index=index)
+    _sync(T)
+    assert np.array_equal(to_host(rn), rhat)
+    assert bf16_close(to_host(dw), w)

@@ -361,6 +361,10 @@ def test_copes_step_composition(orc):
     a = step_in_order([0, 1, 2, 3])
     b = step_in_order([3, 1, 0, 2])
     assert np.array_equal(a, b)
+    c = w0.copy()                                         # the one-call form of the same step
+    orc.update_step(c, offsets, seeds, [1] * N, np.repeat(np.arange(K), Nk), rhat, f32(5e-4), [f32(2e-3)] * K,
+                    orc.SCALE_ALPHA_OVER_N, index=index)
+    assert np.array_equal(a, c)
     ref = w0.astype(np.longdouble).copy()
     for k in range(K):
         pos = index[offsets[k]:offsets[k + 1]]
@@ -371,3 +375,22 @@ def test_copes_step_composition(orc):
         ref[pos] += np.longdouble(float(f32(5e-4))) * g / Nk
     err = np.abs(a.astype(np.longdouble) - ref) / np.spacing(np.abs(ref.astype(np.float32)))
     assert np.max(err) <= 1.0
+
+
+def test_update_step_k1_is_standard_es_and_skips_empty_subspaces(orc):
+    """K = 1 with alpha / N is Eq. 6; a subspace without members is unchanged."""
+    d, N = 300, 6
+    w0 = S.host_weights(d, S.F32, 60)
+    seeds = list(range(7, 7 + N))
+    rhat, _ = orc.normalize(S.rewards("uniform", N, 8), orc.NORM_Z)
+    a = w0.copy()
+    orc.update_step(a, [0, d], seeds, [1] * N, [0] * N, rhat, f32(5e-4), [f32(1e-3)], orc.SCALE_ALPHA_OVER_N)
+    b = w0.copy()
+    orc.update(b, 0, d, seeds, [1] * N, rhat, f32(5e-4), f32(1e-3), orc.SCALE_ALPHA_OVER_N)
+    assert np.array_equal(a, b)
+    eps = np.stack([orc.normals(s, 0, d).astype(np.longdouble) for s in seeds])
+    ref = w0.astype(np.longdouble) + np.longdouble(float(f32(5e-4))) / N * (rhat.astype(np.longdouble) @ eps)
+    assert np.max(np.abs(a.astype(np.longdouble) - ref) / np.spacing(np.abs(ref.astype(np.float32)))) <= 1.0
+    c = w0.copy()
+    orc.update_step(c, [0, 100, 200, 300], seeds, [1] * N, [0, 0, 2, 2, 0, 2], rhat, f32(5e-4), [f32(2e-3)] * 3)
+    assert np.array_equal(c[100:200], w0[100:200]) and not np.array_equal(c[:100], w0[:100])
