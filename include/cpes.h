@@ -29,9 +29,15 @@
  *
  * Weights are a flat buffer of `numel` elements of dtype CPES_BF16 or
  * CPES_F32.  A subspace (cpes_subspace) lists `length` positions j = 0 ..
- * length-1; position j is parameter `offset + j` (index == NULL) or parameter
- * `index[offset + j]` (index = device array of int64 parameter indices, the
- * embedding P_k of Eq. 8).  Index entries outside [0, numel) are skipped.
+ * length-1 -- the embedding P_k of Eq. 8.  Position j is parameter
+ *   offset + j                                  (index == NULL),
+ *   index[offset + j]                           (index != NULL, chunk == 0), or
+ *   index[offset + j / chunk] * chunk + j % chunk
+ *                                               (index != NULL, chunk > 0:
+ *                                                the map names chunks of `chunk`
+ *                                                consecutive parameters),
+ * index being a device array of int64.  Entries that would address outside
+ * [0, numel) are skipped.
  *
  * Noise.  Position j of the noise of a member with seed s is
  *   eps_j = BoxMuller(Philox4x32-10(counter = (lo32 q, hi32 q, 0, 0),
@@ -51,7 +57,7 @@
 extern "C" {
 #endif
 
-#define CPES_ABI_VERSION 1
+#define CPES_ABI_VERSION 2
 
 /* Exported symbols (the library is built with hidden default visibility). */
 #define CPES_API __attribute__((visibility("default")))
@@ -81,7 +87,8 @@ enum cpes_scale_mode { CPES_SCALE_ALPHA_OVER_N_SIGMA = 0, CPES_SCALE_ALPHA_OVER_
 typedef struct cpes_subspace {
     int64_t offset;        /* first parameter (index == NULL) or first map entry */
     int64_t length;        /* number of positions d_k, >= 0 */
-    const int64_t* index;  /* NULL, or device int64 map read at [offset, offset + length) */
+    const int64_t* index;  /* NULL, or device int64 map (parameters or chunk ids) */
+    int64_t chunk;         /* 0, or a power of two >= 8: index entries name chunks of this size */
 } cpes_subspace;
 
 /*
@@ -116,6 +123,31 @@ CPES_API int cpes_partition(int mode, int64_t d, int32_t K, uint64_t seed, const
 
 /* Workspace bytes cpes_partition needs (0 for CONTIGUOUS); 0 for invalid arguments. */
 CPES_API size_t cpes_partition_workspace_bytes(int mode, int64_t d, int32_t K);
+
+/*
+ * cpes_partition_chunks -- the chunk-granular random partition the paper runs
+ * (Sec. 3.3; Supp. A.8 "Partition Replay": chunk-to-subspace assignments
+ * replayed from a stored seed).  The d parameters form n_chunks = ceil(d /
+ * chunk) chunks of `chunk` consecutive parameters (the last may be shorter);
+ * chunk c belongs to subspace floor(E(c) K / n_chunks), E being the keyed
+ * permutation of cpes_partition (CPES_PART_PERMUTATION) on [0, n_chunks).
+ *   chunks_dev (device int64[n_chunks]) receives the chunk ids of each
+ *   subspace, ascending, at [list_offsets[k], list_offsets[k+1]);
+ *   list_offsets_host[k] = ceil(k n_chunks / K) (host, K+1);
+ *   lengths_host[k] = parameters in subspace k (host, K; they sum to d).
+ * Subspace k is then cpes_subspace{list_offsets[k], lengths[k], chunks_dev,
+ * chunk}: every 16-byte unit is contiguous, so kernels stream it at full
+ * bandwidth.  chunk must be a power of two, 8 <= chunk <= 2^30; 1 <= K <=
+ * min(n_chunks, CPES_MAX_PERMUTATION_K); workspace as
+ * cpes_partition_chunks_workspace_bytes(); status_dev as cpes_partition.
+ */
+CPES_API int cpes_partition_chunks(int64_t d, int64_t chunk, int32_t K, uint64_t seed,
+                                   int64_t* list_offsets_host, int64_t* lengths_host, int64_t* chunks_dev,
+                                   void* workspace_dev, size_t workspace_bytes, int32_t* status_dev,
+                                   void* stream);
+
+/* Workspace bytes cpes_partition_chunks needs; 0 for invalid arguments. */
+CPES_API size_t cpes_partition_chunks_workspace_bytes(int64_t d, int64_t chunk, int32_t K);
 
 /*
  * cpes_perturb -- theta_{k,i} = theta + sigma_k P_k eps_{k,i} (Eq. 8, Alg. 1),
@@ -224,6 +256,9 @@ CPES_API int cpes_update(void* w_dev, int64_t numel, int dtype, const cpes_subsp
  *   offsets[k+1]) -- parameters themselves (index_dev == NULL; offsets[K] <=
  *   numel) or entries of the int64 device map index_dev (e.g. the output of
  *   cpes_partition).  Noise position j is counted from offsets[k].
+ *   With chunk > 0, index_dev holds chunk ids (cpes_partition_chunks),
+ *   subspace k is cpes_subspace{offsets[k], lengths_host[k], index_dev, chunk}
+ *   and lengths_host (host, K) is required; otherwise lengths_host is ignored.
  * seeds_host / signs_host / subspace_host (host, n entries): member i has seed,
  *   sign +-1 and the subspace it perturbed; rnorm_dev (device float32[n]) its
  *   standardised reward (joint or per group, cpes_normalize_rewards).
@@ -238,7 +273,8 @@ CPES_API int cpes_update(void* w_dev, int64_t numel, int dtype, const cpes_subsp
  *   CPES_MAX_STEP_SUBSPACES or n above CPES_MAX_MEMBERS -> CPES_ERR_UNSUPPORTED.
  */
 CPES_API int cpes_update_step(void* w_dev, int64_t numel, int dtype, int32_t K, const int64_t* offsets_host,
-                              const int64_t* index_dev, int32_t n, const uint64_t* seeds_host,
+                              const int64_t* index_dev, int64_t chunk, const int64_t* lengths_host,
+                              int32_t n, const uint64_t* seeds_host,
                               const int8_t* signs_host, const int32_t* subspace_host, const float* rnorm_dev,
                               float alpha, const float* sigma_host, int scale_mode, void* stream);
 

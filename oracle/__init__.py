@@ -81,6 +81,7 @@ def lib() -> ctypes.CDLL:
         L.orc_bucket.argtypes = [u64, i64, ctypes.c_int32, i64]
         L.orc_bucket.restype = ctypes.c_int32
         L.orc_partition.argtypes = [i32, i64, ctypes.c_int32, u64, vp, vp, vp]
+        L.orc_partition_chunks.argtypes = [i64, i64, ctypes.c_int32, u64, vp, vp, vp]
         L.orc_num_threads.restype = i32
         _lib = L
     return _lib
@@ -243,6 +244,22 @@ def partition(mode, d, K, seed=0, bounds=None, with_index=True):
     index = np.empty(d, dtype=np.int64) if (mode == PART_PERMUTATION and with_index) else None
     _check(lib().orc_partition(mode, d, K, seed, _ptr(b), _ptr(offsets), _ptr(index)), "partition")
     return offsets, index
+
+
+def partition_chunks(d, chunk, K, seed):
+    """Returns (list_offsets[K+1], lengths[K], chunk ids grouped by subspace)."""
+    n_chunks = -(-d // chunk)
+    offs = np.empty(K + 1, dtype=np.int64)
+    lens = np.empty(K, dtype=np.int64)
+    chunks = np.empty(n_chunks, dtype=np.int64)
+    _check(lib().orc_partition_chunks(d, chunk, K, seed, _ptr(offs), _ptr(lens), _ptr(chunks)), "partition_chunks")
+    return offs, lens, chunks
+
+
+def expand_chunks(chunks, list_offset, length, chunk):
+    """Element map of a chunked subspace: position j -> chunks[list_offset + j // chunk] * chunk + j % chunk."""
+    j = np.arange(length, dtype=np.int64)
+    return chunks[list_offset + j // chunk] * chunk + j % chunk
 
 
 def num_threads() -> int:

@@ -539,6 +539,30 @@ int orc_partition(int mode, int64_t d, int32_t K, uint64_t seed, const int64_t* 
     return ok ? ORC_OK : ORC_ERR;
 }
 
+/* Chunk-granular partition (Sec. 3.3; Supp. A.8 "Partition Replay"): the d
+ * parameters form ceil(d / chunk) chunks of `chunk` consecutive parameters
+ * (the last may be shorter), and the chunk ids are partitioned exactly as
+ * elements are above.  lengths[k] is the number of parameters in the chunks
+ * of subspace k. */
+int orc_partition_chunks(int64_t d, int64_t chunk, int32_t K, uint64_t seed, int64_t* list_offsets,
+                         int64_t* lengths, int64_t* chunks)
+{
+    if (d < 1 || chunk < 1) return ORC_ERR;
+    int64_t n_chunks = (d + chunk - 1) / chunk;
+    int rc = orc_partition(ORC_PART_PERMUTATION, n_chunks, K, seed, NULL, list_offsets, chunks);
+    if (rc != ORC_OK) return rc;
+    for (int k = 0; k < K; ++k) {
+        int64_t total = 0;
+        for (int64_t t = list_offsets[k]; t < list_offsets[k + 1]; ++t) {
+            int64_t first = chunks[t] * chunk;
+            int64_t last = first + chunk < d ? first + chunk : d;
+            total += last - first;
+        }
+        lengths[k] = total;
+    }
+    return ORC_OK;
+}
+
 int orc_num_threads(void)
 {
 #ifdef _OPENMP

@@ -64,6 +64,8 @@ int64_t orc_prp(uint64_t seed, int64_t d, int64_t x);
 int32_t orc_bucket(uint64_t seed, int64_t d, int32_t K, int64_t i);
 int orc_partition(int mode, int64_t d, int32_t K, uint64_t seed, const int64_t* bounds,
                   int64_t* offsets, int64_t* index);
+int orc_partition_chunks(int64_t d, int64_t chunk, int32_t K, uint64_t seed, int64_t* list_offsets,
+                         int64_t* lengths, int64_t* chunks);
 int orc_num_threads(void);
 
 #endif

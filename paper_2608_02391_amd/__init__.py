@@ -24,7 +24,8 @@ SCALE_ALPHA_OVER_N_SIGMA, SCALE_ALPHA_OVER_N = 0, 1
 MAX_MEMBERS, MAX_REWARDS, MAX_GROUPS, MAX_PERMUTATION_K, MAX_STEP_SUBSPACES = 256, 4096, 1024, 256, 32
 
 EXPORTED = (
-    "cpes_partition", "cpes_partition_workspace_bytes", "cpes_perturb", "cpes_restore",
+    "cpes_partition", "cpes_partition_workspace_bytes", "cpes_partition_chunks",
+    "cpes_partition_chunks_workspace_bytes", "cpes_perturb", "cpes_restore",
     "cpes_stage_master", "cpes_normalize_rewards", "cpes_update", "cpes_update_step", "cpes_debug_philox",
     "cpes_debug_normals", "cpes_debug_bm_grid", "cpes_debug_prp", "cpes_rng_probe",
     "cpes_last_error", "cpes_abi_version",
@@ -38,7 +39,8 @@ class CpesError(RuntimeError):
 
 
 class Subspace(ctypes.Structure):
-    _fields_ = [("offset", ctypes.c_int64), ("length", ctypes.c_int64), ("index", ctypes.c_void_p)]
+    _fields_ = [("offset", ctypes.c_int64), ("length", ctypes.c_int64), ("index", ctypes.c_void_p),
+                ("chunk", ctypes.c_int64)]
 
 
 _lib = None
@@ -58,12 +60,14 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     sig = {
         "cpes_partition": [i32, i64, i32, u64, vp, vp, vp, vp, ctypes.c_size_t, vp, vp],
         "cpes_partition_workspace_bytes": [i32, i64, i32],
+        "cpes_partition_chunks": [i64, i64, i32, u64, vp, vp, vp, vp, ctypes.c_size_t, vp, vp],
+        "cpes_partition_chunks_workspace_bytes": [i64, i64, i32],
         "cpes_perturb": [vp, i64, i32, sp, f32, u64, i32, vp, i32, vp],
         "cpes_restore": [vp, i64, i32, sp, f32, u64, i32, vp, i32, vp],
         "cpes_stage_master": [vp, i64, i32, sp, vp, vp],
         "cpes_normalize_rewards": [vp, i32, i32, vp, i32, vp, vp, vp],
         "cpes_update": [vp, i64, i32, sp, vp, i32, vp, vp, vp, f32, f32, i32, vp],
-        "cpes_update_step": [vp, i64, i32, i32, vp, vp, i32, vp, vp, vp, vp, f32, vp, i32, vp],
+        "cpes_update_step": [vp, i64, i32, i32, vp, vp, i64, vp, i32, vp, vp, vp, vp, f32, vp, i32, vp],
         "cpes_debug_philox": [u64, u32, u64, i64, vp, vp],
         "cpes_debug_normals": [u64, i64, i64, vp, vp],
         "cpes_debug_bm_grid": [u32, i64, vp, vp, vp, vp],
@@ -77,6 +81,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         fn.argtypes = args
         fn.restype = ctypes.c_int
     L.cpes_partition_workspace_bytes.restype = ctypes.c_size_t
+    L.cpes_partition_chunks_workspace_bytes.restype = ctypes.c_size_t
     L.cpes_last_error.restype = ctypes.c_char_p
     _lib = L
     return L
@@ -126,11 +131,14 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
-def subspace(offset: int, length: int, index=None) -> Subspace:
-    """Positions j < length at parameter offset + j, or index[offset + j]."""
+def subspace(offset: int, length: int, index=None, chunk: int = 0) -> Subspace:
+    """Positions j < length at parameter offset + j, index[offset + j], or
+    (chunk > 0) index[offset + j // chunk] * chunk + j % chunk."""
     if index is not None and index.dtype != _torch().int64:
         raise TypeError("index map must be int64")
-    return Subspace(int(offset), int(length), _dev_ptr(index, "index map"))
+    sub = Subspace(int(offset), int(length), _dev_ptr(index, "index map"), int(chunk))
+    sub._index = index      # the descriptor holds a raw pointer: keep the map's storage alive with it
+    return sub
 
 
 # ------------------------------------------------------------- entry points --
@@ -150,6 +158,22 @@ def cpes_partition(mode: int, d: int, K: int, seed: int = 0, bounds: Optional[Se
 
 def cpes_partition_workspace_bytes(mode: int, d: int, K: int) -> int:
     return int(load().cpes_partition_workspace_bytes(mode, d, K))
+
+
+def cpes_partition_chunks(d: int, chunk: int, K: int, seed: int, chunks, workspace, status=None, stream=None):
+    """Chunk-granular random partition; returns (list_offsets[K+1], lengths[K])."""
+    L = load()
+    offs = (ctypes.c_int64 * (K + 1))()
+    lens = (ctypes.c_int64 * K)()
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(L.cpes_partition_chunks(d, chunk, K, seed, offs, lens, _dev_ptr(chunks, "chunks"),
+                                   _dev_ptr(workspace, "workspace"), ws_bytes, _dev_ptr(status, "status"),
+                                   _stream(stream)))
+    return [int(x) for x in offs], [int(x) for x in lens]
+
+
+def cpes_partition_chunks_workspace_bytes(d: int, chunk: int, K: int) -> int:
+    return int(load().cpes_partition_chunks_workspace_bytes(d, chunk, K))
 
 
 def cpes_perturb(w, s: Subspace, sigma: float, seed: int, sign: int, aux=None, aux_mode: int = AUX_NONE,
@@ -190,7 +214,8 @@ def cpes_update(w, s: Subspace, seeds: Sequence[int], signs: Sequence[int], rnor
 
 def cpes_update_step(w, offsets: Sequence[int], seeds: Sequence[int], signs: Sequence[int],
                      subspaces: Sequence[int], rnorm, alpha: float, sigmas: Sequence[float],
-                     scale_mode: int = SCALE_ALPHA_OVER_N_SIGMA, index=None, stream=None) -> None:
+                     scale_mode: int = SCALE_ALPHA_OVER_N_SIGMA, index=None, chunk: int = 0,
+                     lengths: Optional[Sequence[int]] = None, stream=None) -> None:
     """Update every subspace of a partition with its own members (one launch)."""
     K = len(offsets) - 1
     n = len(seeds)
@@ -203,8 +228,10 @@ def cpes_update_step(w, offsets: Sequence[int], seeds: Sequence[int], signs: Seq
     csg = (ctypes.c_float * K)(*[float(x) for x in sigmas])
     if index is not None and index.dtype != _torch().int64:
         raise TypeError("index map must be int64")
-    _check(load().cpes_update_step(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), K, co, _dev_ptr(index, "index"), n,
-                                   cs, cg, ck, _dev_ptr(rnorm, "rnorm"), alpha, csg, scale_mode, _stream(stream)))
+    cl = None if lengths is None else (ctypes.c_int64 * K)(*[int(x) for x in lengths])
+    _check(load().cpes_update_step(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), K, co, _dev_ptr(index, "index"),
+                                   int(chunk), cl, n, cs, cg, ck, _dev_ptr(rnorm, "rnorm"), alpha, csg, scale_mode,
+                                   _stream(stream)))
 
 
 def cpes_debug_philox(seed: int, domain: int, q0: int, nblocks: int, out, stream=None) -> None:

@@ -58,7 +58,26 @@ int check_subspace(const void* w, int64_t numel, int dtype, const cpes_subspace*
     if (!s->index && s->offset + s->length > numel)
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: range [%lld, %lld) exceeds numel %lld", fn, (long long)s->offset,
                     (long long)(s->offset + s->length), (long long)numel);
+    if (s->chunk != 0) {
+        if (!s->index) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: a chunked subspace needs its chunk map", fn);
+        if (s->chunk < 8 || s->chunk > ((int64_t)1 << 30) || (s->chunk & (s->chunk - 1)) != 0)
+            return fail(CPES_ERR_INVALID_ARGUMENT, "%s: chunk %lld is not a power of two in [8, 2^30]", fn,
+                        (long long)s->chunk);
+    }
     return CPES_OK;
+}
+
+int addr_mode(const cpes_subspace* s)
+{
+    if (!s->index) return cpes::kAddrContig;
+    return s->chunk ? cpes::kAddrChunk : cpes::kAddrGather;
+}
+
+int log2_exact(int64_t x)
+{
+    int b = 0;
+    while (((int64_t)1 << b) < x) ++b;
+    return b;
 }
 
 int check_sign(int32_t sign, const char* fn)
@@ -77,7 +96,9 @@ int check_sigma(float sigma, const char* fn)
 // Whether the 16-byte vector path applies: every unit's vectors are aligned.
 bool vector_ok(const void* w, int dtype, const cpes_subspace* s, const void* aux, bool aux_is_master)
 {
-    if (s->index) {
+    if (s->index && s->chunk) {
+        if (!aligned16(w)) return false;                    // chunk starts are multiples of 8 elements
+    } else if (s->index) {
         if (!aligned16(s->index + s->offset)) return false;
     } else {
         const char* base = static_cast<const char*>(w) + (size_t)s->offset * elem_size(dtype);
@@ -101,7 +122,40 @@ cpes::StreamArgs stream_args(void* w, int64_t numel, const cpes_subspace* s, con
     a.k0 = (uint32_t)seed;
     a.k1 = (uint32_t)(seed >> 32);
     a.scale = scale;
+    a.chunk_shift = s->chunk ? log2_exact(s->chunk) : 0;
     return a;
+}
+
+// Host replay of the partition permutation (the same definition the device
+// kernels implement), used to find the subspace of one chunk.
+void host_philox(uint32_t c[4], uint32_t k0, uint32_t k1)
+{
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t pa = (uint64_t)0xD2511F53u * c[0];
+        const uint64_t pb = (uint64_t)0xCD9E8D57u * c[2];
+        const uint32_t n0 = (uint32_t)(pb >> 32) ^ c[1] ^ k0;
+        const uint32_t n2 = (uint32_t)(pa >> 32) ^ c[3] ^ k1;
+        c[1] = (uint32_t)pb;
+        c[3] = (uint32_t)pa;
+        c[0] = n0;
+        c[2] = n2;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+}
+
+uint64_t host_feistel(uint64_t seed, int h, uint64_t x)
+{
+    const uint64_t mask = (1ull << h) - 1ull;
+    uint64_t L = x >> h, R = x & mask;
+    for (uint32_t r = 0; r < 8; ++r) {
+        uint32_t c[4] = {(uint32_t)R, r, 3u, 0u};
+        host_philox(c, (uint32_t)seed, (uint32_t)(seed >> 32));
+        const uint64_t nr = L ^ ((uint64_t)c[0] & mask);
+        L = R;
+        R = nr;
+    }
+    return (L << h) | R;
 }
 
 int feistel_half_bits(int64_t d)
@@ -210,6 +264,45 @@ int cpes_partition(int mode, int64_t d, int32_t K, uint64_t seed, const int64_t*
     return hip_status(cpes::launch_partition(a, (hipStream_t)stream), fn);
 }
 
+size_t cpes_partition_chunks_workspace_bytes(int64_t d, int64_t chunk, int32_t K)
+{
+    if (d < 1 || chunk < 8 || chunk > ((int64_t)1 << 30) || (chunk & (chunk - 1)) != 0) return 0;
+    const int64_t n_chunks = (d + chunk - 1) / chunk;
+    return cpes_partition_workspace_bytes(CPES_PART_PERMUTATION, n_chunks, K);
+}
+
+int cpes_partition_chunks(int64_t d, int64_t chunk, int32_t K, uint64_t seed, int64_t* list_offsets_host,
+                          int64_t* lengths_host, int64_t* chunks_dev, void* workspace_dev, size_t workspace_bytes,
+                          int32_t* status_dev, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_partition_chunks";
+    if (d < 1 || d >= ((int64_t)1 << 62)) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: d %lld out of range", fn, (long long)d);
+    if (chunk < 8 || chunk > ((int64_t)1 << 30) || (chunk & (chunk - 1)) != 0)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: chunk %lld is not a power of two in [8, 2^30]", fn, (long long)chunk);
+    if (!list_offsets_host || !lengths_host) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: null host outputs", fn);
+    const int64_t n_chunks = (d + chunk - 1) / chunk;
+    if (K < 1 || (int64_t)K > n_chunks)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: K %d not in [1, %lld chunks]", fn, K, (long long)n_chunks);
+    // the chunk permutation is the permutation partition of the chunk ids
+    int rc = cpes_partition(CPES_PART_PERMUTATION, n_chunks, K, seed, nullptr, list_offsets_host, chunks_dev,
+                            workspace_dev, workspace_bytes, status_dev, stream);
+    if (rc) {
+        const std::string msg = g_error;
+        return fail(rc, "%s: %s", fn, msg.c_str());
+    }
+    for (int32_t k = 0; k < K; ++k) lengths_host[k] = (list_offsets_host[k + 1] - list_offsets_host[k]) * chunk;
+    const int64_t short_by = n_chunks * chunk - d;
+    if (short_by > 0) {   // the last chunk is short; find its subspace
+        const int h = feistel_half_bits(n_chunks);
+        uint64_t y = host_feistel(seed, h, (uint64_t)(n_chunks - 1));
+        while (y >= (uint64_t)n_chunks) y = host_feistel(seed, h, y);
+        const int32_t k = (int32_t)((y * (uint64_t)K) / (uint64_t)n_chunks);
+        lengths_host[k] -= short_by;
+    }
+    return CPES_OK;
+}
+
 int cpes_perturb(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float sigma, uint64_t seed,
                  int32_t sign, void* aux_dev, int aux_mode, void* stream)
 {
@@ -229,7 +322,7 @@ int cpes_perturb(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, 
     const void* aux = aux_mode == CPES_AUX_NONE ? nullptr : aux_dev;
     const bool vec = vector_ok(w_dev, dtype, s, aux, aux_mode == CPES_AUX_MASTER);
     const cpes::StreamArgs a = stream_args(w_dev, numel, s, aux, seed, scale);
-    return hip_status(cpes::launch_perturb(dtype, aux_mode, s->index != nullptr, vec, a, (hipStream_t)stream), fn);
+    return hip_status(cpes::launch_perturb(dtype, aux_mode, addr_mode(s), vec, a, (hipStream_t)stream), fn);
 }
 
 int cpes_restore(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float sigma, uint64_t seed,
@@ -249,17 +342,17 @@ int cpes_restore(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, 
     if (aux_mode == CPES_AUX_MASTER && dtype != CPES_BF16)
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: master source needs bf16 weights", fn);
     if (s->length == 0) return CPES_OK;
-    const bool gather = s->index != nullptr;
+    const int addr = addr_mode(s);
     hipStream_t st = (hipStream_t)stream;
     if (aux_mode == CPES_AUX_NONE) {
         const float scale = sign > 0 ? -sigma : sigma;
         const cpes::StreamArgs a = stream_args(w_dev, numel, s, nullptr, seed, scale);
-        return hip_status(cpes::launch_perturb(dtype, cpes::kAuxNone, gather, vector_ok(w_dev, dtype, s, nullptr, false), a, st), fn);
+        return hip_status(cpes::launch_perturb(dtype, cpes::kAuxNone, addr, vector_ok(w_dev, dtype, s, nullptr, false), a, st), fn);
     }
     const cpes::StreamArgs a = stream_args(w_dev, numel, s, aux_dev, seed, 0.0f);
     const bool vec = vector_ok(w_dev, dtype, s, aux_dev, aux_mode == CPES_AUX_MASTER);
-    if (aux_mode == CPES_AUX_SNAPSHOT) return hip_status(cpes::launch_restore_copy(dtype, gather, vec, a, st), fn);
-    return hip_status(cpes::launch_restore_master(gather, vec, a, st), fn);
+    if (aux_mode == CPES_AUX_SNAPSHOT) return hip_status(cpes::launch_restore_copy(dtype, addr, vec, a, st), fn);
+    return hip_status(cpes::launch_restore_master(addr, vec, a, st), fn);
 }
 
 int cpes_stage_master(const void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float* master_dev,
@@ -273,7 +366,7 @@ int cpes_stage_master(const void* w_dev, int64_t numel, int dtype, const cpes_su
     if (s->length == 0) return CPES_OK;
     const bool vec = vector_ok(w_dev, dtype, s, master_dev, true);
     const cpes::StreamArgs a = stream_args(const_cast<void*>(w_dev), numel, s, master_dev, 0, 0.0f);
-    return hip_status(cpes::launch_stage_master(dtype, s->index != nullptr, vec, a, (hipStream_t)stream), fn);
+    return hip_status(cpes::launch_stage_master(dtype, addr_mode(s), vec, a, (hipStream_t)stream), fn);
 }
 
 int cpes_normalize_rewards(const float* r_dev, int32_t n, int mode, const int32_t* group_dev, int32_t n_groups,
@@ -348,12 +441,14 @@ int cpes_update(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, f
     a.step = (float)step;
     a.n_members = n;
     a.n_streams = n_streams;
+    a.chunk_shift = s->chunk ? log2_exact(s->chunk) : 0;
     const bool vec = vector_ok(w_dev, dtype, s, master_dev, true);
-    return hip_status(cpes::launch_update(dtype, master_dev != nullptr, s->index != nullptr, vec, a, (hipStream_t)stream), fn);
+    return hip_status(cpes::launch_update(dtype, master_dev != nullptr, addr_mode(s), vec, a, (hipStream_t)stream), fn);
 }
 
 int cpes_update_step(void* w_dev, int64_t numel, int dtype, int32_t K, const int64_t* offsets_host,
-                     const int64_t* index_dev, int32_t n, const uint64_t* seeds_host, const int8_t* signs_host,
+                     const int64_t* index_dev, int64_t chunk, const int64_t* lengths_host, int32_t n,
+                     const uint64_t* seeds_host, const int8_t* signs_host,
                      const int32_t* subspace_host, const float* rnorm_dev, float alpha, const float* sigma_host,
                      int scale_mode, void* stream)
 {
@@ -371,6 +466,15 @@ int cpes_update_step(void* w_dev, int64_t numel, int dtype, int32_t K, const int
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown scale_mode %d", fn, scale_mode);
     if (!std::isfinite(alpha)) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: alpha is not finite", fn);
     if (offsets_host[0] < 0) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: offsets[0] < 0", fn);
+    if (chunk != 0) {
+        if (!index_dev || !lengths_host)
+            return fail(CPES_ERR_INVALID_ARGUMENT, "%s: chunked subspaces need the chunk map and lengths", fn);
+        if (chunk < 8 || chunk > ((int64_t)1 << 30) || (chunk & (chunk - 1)) != 0)
+            return fail(CPES_ERR_INVALID_ARGUMENT, "%s: chunk %lld is not a power of two in [8, 2^30]", fn, (long long)chunk);
+        for (int32_t k = 0; k < K; ++k)
+            if (lengths_host[k] < 0 || lengths_host[k] > (offsets_host[k + 1] - offsets_host[k]) * chunk)
+                return fail(CPES_ERR_INVALID_ARGUMENT, "%s: length of subspace %d does not fit its chunks", fn, k);
+    }
     for (int32_t k = 0; k < K; ++k)
         if (offsets_host[k + 1] < offsets_host[k]) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: offsets decrease at %d", fn, k);
     if (!index_dev && offsets_host[K] > numel)
@@ -419,13 +523,16 @@ int cpes_update_step(void* w_dev, int64_t numel, int dtype, int32_t K, const int
         a.offset[k] = offsets_host[k];
         a.tile_begin[k] = tiles;
         if (k == K) break;
-        const int64_t len = offsets_host[k + 1] - offsets_host[k];
+        const int64_t len = chunk ? lengths_host[k] : offsets_host[k + 1] - offsets_host[k];
+        a.length[k] = len;
         const int64_t units = (len + N - 1) / N;
         if (count[k] > 0) tiles += (units + 63) / 64;   // subspaces without members are left alone
-        const void* first = index_dev ? (const void*)(index_dev + offsets_host[k])
+        const void* first = chunk ? w_dev
+                          : index_dev ? (const void*)(index_dev + offsets_host[k])
                                       : (const void*)(static_cast<const char*>(w_dev) + (size_t)offsets_host[k] * elem_size(dtype));
         if (aligned16(first)) a.vec_mask |= 1u << k;
     }
+    a.chunk_shift = chunk ? log2_exact(chunk) : 0;
     a.w = w_dev;
     a.index = index_dev;
     a.rnorm = rnorm_dev;
@@ -434,7 +541,8 @@ int cpes_update_step(void* w_dev, int64_t numel, int dtype, int32_t K, const int
     a.n_members = n;
     a.n_streams = n_streams;
     if (tiles == 0) return CPES_OK;
-    return hip_status(cpes::launch_update_step(dtype, index_dev != nullptr, a, (hipStream_t)stream), fn);
+    const int addr = !index_dev ? cpes::kAddrContig : chunk ? cpes::kAddrChunk : cpes::kAddrGather;
+    return hip_status(cpes::launch_update_step(dtype, addr, a, (hipStream_t)stream), fn);
 }
 
 int cpes_debug_philox(uint64_t seed, uint32_t domain, uint64_t q0, int64_t nblocks, uint32_t* out_dev, void* stream)

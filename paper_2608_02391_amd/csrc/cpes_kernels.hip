@@ -79,17 +79,52 @@ __device__ __forceinline__ void load_index(const int64_t* p, int64_t v[N])
 __device__ __forceinline__ int64_t grid_stride() { return (int64_t)gridDim.x * blockDim.x; }
 __device__ __forceinline__ int64_t global_tid() { return (int64_t)blockIdx.x * blockDim.x + threadIdx.x; }
 
+// Subspace addressing: position j is parameter offset + j (kContig),
+// index[offset + j] (kGather), or, with chunks of 2^s parameters,
+// index[offset + (j >> s)] * 2^s + (j mod 2^s) (kChunk).
+constexpr int kContig = kAddrContig, kGather = kAddrGather, kChunk = kAddrChunk;
+
 // Resolve the parameter index of position j; returns false for a map entry
 // outside [0, numel) (skipped, never dereferenced).
-template <bool GATHER>
-__device__ __forceinline__ bool param_of(const StreamArgs& a, int64_t j, int64_t& i)
+template <int ADDR>
+__device__ __forceinline__ bool param_at(const int64_t* index, int64_t offset, int64_t numel, int shift, int64_t j,
+                                         int64_t& i)
 {
-    if (!GATHER) {
-        i = a.offset + j;
+    if (ADDR == kContig) {
+        i = offset + j;
         return true;
     }
-    i = a.index[a.offset + j];
-    return i >= 0 && i < a.numel;
+    if (ADDR == kGather) {
+        i = index[offset + j];
+        return i >= 0 && i < numel;
+    }
+    const int64_t c = index[offset + (j >> shift)];
+    if (c < 0 || c > (numel >> shift)) return false;
+    i = (c << shift) + (j & ((1ll << shift) - 1));
+    return i < numel;
+}
+
+template <int ADDR>
+__device__ __forceinline__ bool param_of(const StreamArgs& a, int64_t j, int64_t& i)
+{
+    return param_at<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j, i);
+}
+
+// First parameter of the unit starting at position j0 for contiguous and
+// chunked subspaces (a unit never crosses a chunk); false if the unit would
+// leave [0, numel), in which case the caller takes the element path.
+template <int ADDR>
+__device__ __forceinline__ bool unit_base(const int64_t* index, int64_t offset, int64_t numel, int shift, int64_t j0,
+                                          int n, int64_t& base)
+{
+    if (ADDR == kContig) {
+        base = offset + j0;
+        return true;
+    }
+    const int64_t c = index[offset + (j0 >> shift)];
+    if (c < 0 || c > (numel >> shift)) return false;
+    base = (c << shift) + (j0 & ((1ll << shift) - 1));
+    return base + n <= numel;
 }
 
 // Drive a streaming kernel: every full unit goes through `vec_body` (16-byte
@@ -113,25 +148,53 @@ __device__ __forceinline__ void for_each_unit(int64_t length, VecBody&& vec_body
 // w[p(j)] = cast(fmaf(scale, eps_j, src_j)); src = w (optionally backed up to
 // the snapshot first), the fp32 master, or an existing backup.  Also serves
 // replay restore with scale = -sign * sigma.
-template <typename T, int AUX, bool GATHER, bool VEC>
+template <typename T, int AUX, int ADDR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
 {
     constexpr int N = UnitOf<T>::n;
     T* w = static_cast<T*>(a.w);
+    auto scalar_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+        float z[N];
+        unit_normals<N>(a.k0, a.k1, (uint64_t)j0 >> 2, z);
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+            const int64_t j = j0 + e;
+            int64_t i;
+            if (j >= a.length || !param_of<ADDR>(a, j, i)) continue;
+            float src;
+            if (AUX == kAuxMaster) {
+                src = static_cast<const float*>(a.aux)[j];
+            } else if (AUX == kAuxBackup) {
+                src = to_f32<T>(static_cast<const T*>(a.aux)[j]);
+            } else {
+                const T old = w[i];
+                if (AUX == kAuxSnapshot) static_cast<T*>(a.aux)[j] = old;
+                src = to_f32<T>(old);
+            }
+            w[i] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src));
+        }
+    };
     auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
+        int64_t base = 0;
+        int64_t idx[N];
+        if (ADDR == kGather) {
+            load_index<N>(a.index + a.offset + j0, idx);
+        } else if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+            scalar_body(u);
+            return;
+        }
         float src[N];
         T old[N];
-        int64_t idx[N];
-        if (GATHER) {
-            load_index<N>(a.index + a.offset + j0, idx);
+        if (ADDR == kGather && AUX != kAuxMaster && AUX != kAuxBackup) {
 #pragma unroll
             for (int e = 0; e < N; ++e) {
                 const bool ok = idx[e] >= 0 && idx[e] < a.numel;
                 old[e] = ok ? w[idx[e]] : T(0);
             }
         } else if (AUX != kAuxMaster && AUX != kAuxBackup) {
-            load_vec<T>(w + a.offset + j0, old);
+            load_vec<T>(w + base, old);
         }
         if (AUX == kAuxMaster) {
             load_f32s<N>(static_cast<const float*>(a.aux) + j0, src);
@@ -150,34 +213,12 @@ __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
         T out[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src[e]));
-        if (GATHER) {
+        if (ADDR == kGather) {
 #pragma unroll
             for (int e = 0; e < N; ++e)
                 if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = out[e];
         } else {
-            store_vec<T>(w + a.offset + j0, out);
-        }
-    };
-    auto scalar_body = [&](int64_t u) {
-        const int64_t j0 = u * N;
-        float z[N];
-        unit_normals<N>(a.k0, a.k1, (uint64_t)j0 >> 2, z);
-#pragma unroll
-        for (int e = 0; e < N; ++e) {
-            const int64_t j = j0 + e;
-            int64_t i;
-            if (j >= a.length || !param_of<GATHER>(a, j, i)) continue;
-            float src;
-            if (AUX == kAuxMaster) {
-                src = static_cast<const float*>(a.aux)[j];
-            } else if (AUX == kAuxBackup) {
-                src = to_f32<T>(static_cast<const T*>(a.aux)[j]);
-            } else {
-                const T old = w[i];
-                if (AUX == kAuxSnapshot) static_cast<T*>(a.aux)[j] = old;
-                src = to_f32<T>(old);
-            }
-            w[i] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src));
+            store_vec<T>(w + base, out);
         }
     };
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
@@ -185,45 +226,59 @@ __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
 
 // --------------------------------------------------------------- restores --
 // Snapshot restore: w[p(j)] = snap[j], a bit copy.
-template <typename T, bool GATHER, bool VEC>
+template <typename T, int ADDR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_restore_copy(StreamArgs a)
 {
     constexpr int N = UnitOf<T>::n;
     T* w = static_cast<T*>(a.w);
     const T* snap = static_cast<const T*>(a.aux);
-    auto vec_body = [&](int64_t u) {
-        const int64_t j0 = u * N;
-        T v[N];
-        load_vec<T>(snap + j0, v);
-        if (GATHER) {
-            int64_t idx[N];
-            load_index<N>(a.index + a.offset + j0, idx);
-#pragma unroll
-            for (int e = 0; e < N; ++e)
-                if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = v[e];
-        } else {
-            store_vec<T>(w + a.offset + j0, v);
-        }
-    };
     auto scalar_body = [&](int64_t u) {
         const int64_t j0 = u * N;
 #pragma unroll
         for (int e = 0; e < N; ++e) {
             const int64_t j = j0 + e;
             int64_t i;
-            if (j < a.length && param_of<GATHER>(a, j, i)) w[i] = snap[j];
+            if (j < a.length && param_of<ADDR>(a, j, i)) w[i] = snap[j];
+        }
+    };
+    auto vec_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+        T v[N];
+        load_vec<T>(snap + j0, v);
+        if (ADDR == kGather) {
+            int64_t idx[N];
+            load_index<N>(a.index + a.offset + j0, idx);
+#pragma unroll
+            for (int e = 0; e < N; ++e)
+                if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = v[e];
+        } else {
+            int64_t base;
+            if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+                scalar_body(u);
+                return;
+            }
+            store_vec<T>(w + base, v);
         }
     };
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
 
 // Master restore (bf16 weights): w[p(j)] = rne_bf16(master[j]).
-template <bool GATHER, bool VEC>
+template <int ADDR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_restore_master(StreamArgs a)
 {
     constexpr int N = 8;
     uint16_t* w = static_cast<uint16_t*>(a.w);
     const float* master = static_cast<const float*>(a.aux);
+    auto scalar_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+            const int64_t j = j0 + e;
+            int64_t i;
+            if (j < a.length && param_of<ADDR>(a, j, i)) w[i] = f32_to_bf16(master[j]);
+        }
+    };
     auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
         float m[N];
@@ -231,59 +286,60 @@ __global__ __launch_bounds__(kBlock) void k_restore_master(StreamArgs a)
         uint16_t v[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) v[e] = f32_to_bf16(m[e]);
-        if (GATHER) {
+        if (ADDR == kGather) {
             int64_t idx[N];
             load_index<N>(a.index + a.offset + j0, idx);
 #pragma unroll
             for (int e = 0; e < N; ++e)
                 if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = v[e];
         } else {
-            store_vec<uint16_t>(w + a.offset + j0, v);
-        }
-    };
-    auto scalar_body = [&](int64_t u) {
-        const int64_t j0 = u * N;
-#pragma unroll
-        for (int e = 0; e < N; ++e) {
-            const int64_t j = j0 + e;
-            int64_t i;
-            if (j < a.length && param_of<GATHER>(a, j, i)) w[i] = f32_to_bf16(master[j]);
+            int64_t base;
+            if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+                scalar_body(u);
+                return;
+            }
+            store_vec<uint16_t>(w + base, v);
         }
     };
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
 
 // Master staging: master[j] = f32(w[p(j)]).
-template <typename T, bool GATHER, bool VEC>
+template <typename T, int ADDR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_stage_master(StreamArgs a)
 {
     constexpr int N = UnitOf<T>::n;
     const T* w = static_cast<const T*>(a.w);
     float* master = static_cast<float*>(a.aux);
-    auto vec_body = [&](int64_t u) {
-        const int64_t j0 = u * N;
-        T v[N];
-        if (GATHER) {
-            int64_t idx[N];
-            load_index<N>(a.index + a.offset + j0, idx);
-#pragma unroll
-            for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
-        } else {
-            load_vec<T>(w + a.offset + j0, v);
-        }
-        float m[N];
-#pragma unroll
-        for (int e = 0; e < N; ++e) m[e] = to_f32<T>(v[e]);
-        store_f32s<N>(master + j0, m);
-    };
     auto scalar_body = [&](int64_t u) {
         const int64_t j0 = u * N;
 #pragma unroll
         for (int e = 0; e < N; ++e) {
             const int64_t j = j0 + e;
             int64_t i;
-            if (j < a.length && param_of<GATHER>(a, j, i)) master[j] = to_f32<T>(w[i]);
+            if (j < a.length && param_of<ADDR>(a, j, i)) master[j] = to_f32<T>(w[i]);
         }
+    };
+    auto vec_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+        T v[N];
+        if (ADDR == kGather) {
+            int64_t idx[N];
+            load_index<N>(a.index + a.offset + j0, idx);
+#pragma unroll
+            for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
+        } else {
+            int64_t base;
+            if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+                scalar_body(u);
+                return;
+            }
+            load_vec<T>(w + base, v);
+        }
+        float m[N];
+#pragma unroll
+        for (int e = 0; e < N; ++e) m[e] = to_f32<T>(v[e]);
+        store_f32s<N>(master + j0, m);
     };
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
@@ -292,7 +348,7 @@ __global__ __launch_bounds__(kBlock) void k_stage_master(StreamArgs a)
 // theta_S += step * sum_u c_u eps_u, c_u = sum over members of stream u of
 // sign * rnorm.  Each thread reads its unit of weights once, regenerates every
 // stream's noise for it in registers, accumulates in fp32 and writes once.
-template <typename T, bool MASTER, bool GATHER, bool VEC>
+template <typename T, bool MASTER, int ADDR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
 {
     constexpr int N = MASTER ? 8 : UnitOf<T>::n;
@@ -307,10 +363,6 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
     __syncthreads();
 
     T* w = static_cast<T*>(a.w);
-    StreamArgs sa;
-    sa.index = a.index;
-    sa.offset = a.offset;
-    sa.numel = a.numel;
     auto accumulate = [&](int64_t j0, float acc[N]) {
 #pragma unroll
         for (int e = 0; e < N; ++e) acc[e] = 0.0f;
@@ -322,18 +374,43 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
             for (int e = 0; e < N; ++e) acc[e] = __builtin_fmaf(c, z[e], acc[e]);
         }
     };
+    auto scalar_finish = [&](int64_t j0, const float acc[N]) {
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+            const int64_t j = j0 + e;
+            int64_t i;
+            if (j >= a.length || !param_at<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j, i)) continue;
+            if (MASTER) {
+                const float m = __builtin_fmaf(a.step, acc[e], a.master[j]);
+                a.master[j] = m;
+                w[i] = from_f32<T>(m);
+            } else {
+                w[i] = from_f32<T>(__builtin_fmaf(a.step, acc[e], to_f32<T>(w[i])));
+            }
+        }
+    };
+    auto scalar_body = [&](int64_t u) {
+        float acc[N];
+        accumulate(u * N, acc);
+        scalar_finish(u * N, acc);
+    };
     auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
         float acc[N];
         accumulate(j0, acc);
         int64_t idx[N];
+        int64_t base = 0;
         T v[N];
-        if (GATHER) {
+        if (ADDR == kGather) {
             load_index<N>(a.index + a.offset + j0, idx);
 #pragma unroll
             for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
-        } else if (!MASTER) {
-            load_vec<T>(w + a.offset + j0, v);
+        } else {
+            if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+                scalar_finish(j0, acc);
+                return;
+            }
+            if (!MASTER) load_vec<T>(w + base, v);
         }
         T out[N];
         if (MASTER) {
@@ -349,30 +426,12 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
 #pragma unroll
             for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.step, acc[e], to_f32<T>(v[e])));
         }
-        if (GATHER) {
+        if (ADDR == kGather) {
 #pragma unroll
             for (int e = 0; e < N; ++e)
                 if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = out[e];
         } else {
-            store_vec<T>(w + a.offset + j0, out);
-        }
-    };
-    auto scalar_body = [&](int64_t u) {
-        const int64_t j0 = u * N;
-        float acc[N];
-        accumulate(j0, acc);
-#pragma unroll
-        for (int e = 0; e < N; ++e) {
-            const int64_t j = j0 + e;
-            int64_t i;
-            if (j >= a.length || !param_of<GATHER>(sa, j, i)) continue;
-            if (MASTER) {
-                const float m = __builtin_fmaf(a.step, acc[e], a.master[j]);
-                a.master[j] = m;
-                w[i] = from_f32<T>(m);
-            } else {
-                w[i] = from_f32<T>(__builtin_fmaf(a.step, acc[e], to_f32<T>(w[i])));
-            }
+            store_vec<T>(w + base, out);
         }
     };
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
@@ -383,7 +442,7 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
 // every subspace of the partition with its own members, in one launch.  Units
 // restart at each subspace's first position, so noise position j is always
 // relative to the subspace; each wave works on 64 units of one subspace.
-template <typename T, bool GATHER>
+template <typename T, int ADDR>
 __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
 {
     constexpr int N = UnitOf<T>::n;
@@ -403,8 +462,8 @@ __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
     for (int64_t t = wave; t < tiles; t += waves) {
         int k = 0;
         while (k + 1 < a.K && a.tile_begin[k + 1] <= t) ++k;
-        const int64_t base = a.offset[k];
-        const int64_t len = a.offset[k + 1] - base;
+        const int64_t off = a.offset[k];
+        const int64_t len = a.length[k];
         const int64_t j0 = ((t - a.tile_begin[k]) * 64 + lane) * N;
         if (j0 >= len) continue;
         float acc[N];
@@ -418,32 +477,34 @@ __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
             for (int e = 0; e < N; ++e) acc[e] = __builtin_fmaf(c, z[e], acc[e]);
         }
         const float step = a.step[k];
-        if (((a.vec_mask >> k) & 1u) && j0 + N <= len) {
+        int64_t base = 0;
+        const bool vec = ((a.vec_mask >> k) & 1u) && j0 + N <= len &&
+                         (ADDR == kGather || unit_base<ADDR>(a.index, off, a.numel, a.chunk_shift, j0, N, base));
+        if (vec) {
             T v[N], out[N];
             int64_t idx[N];
-            if (GATHER) {
-                load_index<N>(a.index + base + j0, idx);
+            if (ADDR == kGather) {
+                load_index<N>(a.index + off + j0, idx);
 #pragma unroll
                 for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
             } else {
-                load_vec<T>(w + base + j0, v);
+                load_vec<T>(w + base, v);
             }
 #pragma unroll
             for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(step, acc[e], to_f32<T>(v[e])));
-            if (GATHER) {
+            if (ADDR == kGather) {
 #pragma unroll
                 for (int e = 0; e < N; ++e)
                     if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = out[e];
             } else {
-                store_vec<T>(w + base + j0, out);
+                store_vec<T>(w + base, out);
             }
         } else {
 #pragma unroll
             for (int e = 0; e < N; ++e) {
                 const int64_t j = j0 + e;
-                if (j >= len) continue;
-                const int64_t i = GATHER ? a.index[base + j] : base + j;
-                if (GATHER && (i < 0 || i >= a.numel)) continue;
+                int64_t i;
+                if (j >= len || !param_at<ADDR>(a.index, off, a.numel, a.chunk_shift, j, i)) continue;
                 w[i] = from_f32<T>(__builtin_fmaf(step, acc[e], to_f32<T>(w[i])));
             }
         }
@@ -794,86 +855,106 @@ int64_t units_of(int64_t length)
     return (length + UnitOf<T>::n - 1) / UnitOf<T>::n;
 }
 
+// Instantiate a streaming kernel for the addressing mode and vector flag.
+#define CPES_DISPATCH_ADDR_VEC(KERNEL, ...)                                                          \
+    switch (addr) {                                                                                  \
+    case kGather: return vec ? launch1d(KERNEL<__VA_ARGS__, kGather, true>, u, a, s)                  \
+                             : launch1d(KERNEL<__VA_ARGS__, kGather, false>, u, a, s);                \
+    case kChunk: return vec ? launch1d(KERNEL<__VA_ARGS__, kChunk, true>, u, a, s)                    \
+                            : launch1d(KERNEL<__VA_ARGS__, kChunk, false>, u, a, s);                  \
+    default: return vec ? launch1d(KERNEL<__VA_ARGS__, kContig, true>, u, a, s)                       \
+                        : launch1d(KERNEL<__VA_ARGS__, kContig, false>, u, a, s);                     \
+    }
+
 template <typename T, int AUX>
-hipError_t perturb_t(bool gather, bool vec, const StreamArgs& a, hipStream_t s)
+hipError_t perturb_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
     const int64_t u = units_of<T>(a.length);
-    if (gather) return vec ? launch1d(k_perturb<T, AUX, true, true>, u, a, s) : launch1d(k_perturb<T, AUX, true, false>, u, a, s);
-    return vec ? launch1d(k_perturb<T, AUX, false, true>, u, a, s) : launch1d(k_perturb<T, AUX, false, false>, u, a, s);
+    CPES_DISPATCH_ADDR_VEC(k_perturb, T, AUX)
 }
 
 template <typename T, bool MASTER>
-hipError_t update_t(bool gather, bool vec, const UpdateArgs& a, hipStream_t s)
+hipError_t update_t(int addr, bool vec, const UpdateArgs& a, hipStream_t s)
 {
     const int64_t u = (a.length + (MASTER ? 8 : UnitOf<T>::n) - 1) / (MASTER ? 8 : UnitOf<T>::n);
-    if (gather) return vec ? launch1d(k_update<T, MASTER, true, true>, u, a, s) : launch1d(k_update<T, MASTER, true, false>, u, a, s);
-    return vec ? launch1d(k_update<T, MASTER, false, true>, u, a, s) : launch1d(k_update<T, MASTER, false, false>, u, a, s);
+    CPES_DISPATCH_ADDR_VEC(k_update, T, MASTER)
+}
+
+template <typename T>
+hipError_t restore_copy_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
+{
+    const int64_t u = units_of<T>(a.length);
+    CPES_DISPATCH_ADDR_VEC(k_restore_copy, T)
+}
+
+template <typename T>
+hipError_t stage_master_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
+{
+    const int64_t u = units_of<T>(a.length);
+    CPES_DISPATCH_ADDR_VEC(k_stage_master, T)
+}
+
+hipError_t restore_master_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
+{
+    const int64_t u = (a.length + 7) / 8;
+    switch (addr) {
+    case kGather: return vec ? launch1d(k_restore_master<kGather, true>, u, a, s) : launch1d(k_restore_master<kGather, false>, u, a, s);
+    case kChunk: return vec ? launch1d(k_restore_master<kChunk, true>, u, a, s) : launch1d(k_restore_master<kChunk, false>, u, a, s);
+    default: return vec ? launch1d(k_restore_master<kContig, true>, u, a, s) : launch1d(k_restore_master<kContig, false>, u, a, s);
+    }
+}
+
+template <typename T>
+hipError_t update_step_t(int addr, const StepArgs& a, hipStream_t s)
+{
+    const int64_t blocks = grid_for(a.tile_begin[a.K] * 64);
+    switch (addr) {
+    case kGather: hipLaunchKernelGGL((k_update_step<T, kGather>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
+    case kChunk: hipLaunchKernelGGL((k_update_step<T, kChunk>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
+    default: hipLaunchKernelGGL((k_update_step<T, kContig>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
+    }
+    return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_perturb(int dtype, int aux, bool gather, bool vec, const StreamArgs& a, hipStream_t s)
+hipError_t launch_perturb(int dtype, int aux, int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
     if (dtype == 0) {
-        if (aux == kAuxSnapshot) return perturb_t<uint16_t, kAuxSnapshot>(gather, vec, a, s);
-        if (aux == kAuxMaster) return perturb_t<uint16_t, kAuxMaster>(gather, vec, a, s);
-        if (aux == kAuxBackup) return perturb_t<uint16_t, kAuxBackup>(gather, vec, a, s);
-        return perturb_t<uint16_t, kAuxNone>(gather, vec, a, s);
+        if (aux == kAuxSnapshot) return perturb_t<uint16_t, kAuxSnapshot>(addr, vec, a, s);
+        if (aux == kAuxMaster) return perturb_t<uint16_t, kAuxMaster>(addr, vec, a, s);
+        if (aux == kAuxBackup) return perturb_t<uint16_t, kAuxBackup>(addr, vec, a, s);
+        return perturb_t<uint16_t, kAuxNone>(addr, vec, a, s);
     }
-    if (aux == kAuxSnapshot) return perturb_t<float, kAuxSnapshot>(gather, vec, a, s);
-    if (aux == kAuxBackup) return perturb_t<float, kAuxBackup>(gather, vec, a, s);
-    return perturb_t<float, kAuxNone>(gather, vec, a, s);
+    if (aux == kAuxSnapshot) return perturb_t<float, kAuxSnapshot>(addr, vec, a, s);
+    if (aux == kAuxBackup) return perturb_t<float, kAuxBackup>(addr, vec, a, s);
+    return perturb_t<float, kAuxNone>(addr, vec, a, s);
 }
 
-hipError_t launch_restore_copy(int dtype, bool gather, bool vec, const StreamArgs& a, hipStream_t s)
+hipError_t launch_restore_copy(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
-    if (dtype == 0) {
-        const int64_t u = units_of<uint16_t>(a.length);
-        if (gather) return vec ? launch1d(k_restore_copy<uint16_t, true, true>, u, a, s) : launch1d(k_restore_copy<uint16_t, true, false>, u, a, s);
-        return vec ? launch1d(k_restore_copy<uint16_t, false, true>, u, a, s) : launch1d(k_restore_copy<uint16_t, false, false>, u, a, s);
-    }
-    const int64_t u = units_of<float>(a.length);
-    if (gather) return vec ? launch1d(k_restore_copy<float, true, true>, u, a, s) : launch1d(k_restore_copy<float, true, false>, u, a, s);
-    return vec ? launch1d(k_restore_copy<float, false, true>, u, a, s) : launch1d(k_restore_copy<float, false, false>, u, a, s);
+    return dtype == 0 ? restore_copy_t<uint16_t>(addr, vec, a, s) : restore_copy_t<float>(addr, vec, a, s);
 }
 
-hipError_t launch_restore_master(bool gather, bool vec, const StreamArgs& a, hipStream_t s)
+hipError_t launch_restore_master(int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
-    const int64_t u = (a.length + 7) / 8;
-    if (gather) return vec ? launch1d(k_restore_master<true, true>, u, a, s) : launch1d(k_restore_master<true, false>, u, a, s);
-    return vec ? launch1d(k_restore_master<false, true>, u, a, s) : launch1d(k_restore_master<false, false>, u, a, s);
+    return restore_master_t(addr, vec, a, s);
 }
 
-hipError_t launch_stage_master(int dtype, bool gather, bool vec, const StreamArgs& a, hipStream_t s)
+hipError_t launch_stage_master(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
-    if (dtype == 0) {
-        const int64_t u = units_of<uint16_t>(a.length);
-        if (gather) return vec ? launch1d(k_stage_master<uint16_t, true, true>, u, a, s) : launch1d(k_stage_master<uint16_t, true, false>, u, a, s);
-        return vec ? launch1d(k_stage_master<uint16_t, false, true>, u, a, s) : launch1d(k_stage_master<uint16_t, false, false>, u, a, s);
-    }
-    const int64_t u = units_of<float>(a.length);
-    if (gather) return vec ? launch1d(k_stage_master<float, true, true>, u, a, s) : launch1d(k_stage_master<float, true, false>, u, a, s);
-    return vec ? launch1d(k_stage_master<float, false, true>, u, a, s) : launch1d(k_stage_master<float, false, false>, u, a, s);
+    return dtype == 0 ? stage_master_t<uint16_t>(addr, vec, a, s) : stage_master_t<float>(addr, vec, a, s);
 }
 
-hipError_t launch_update(int dtype, bool master, bool gather, bool vec, const UpdateArgs& a, hipStream_t s)
+hipError_t launch_update(int dtype, bool master, int addr, bool vec, const UpdateArgs& a, hipStream_t s)
 {
-    if (dtype == 0) return master ? update_t<uint16_t, true>(gather, vec, a, s) : update_t<uint16_t, false>(gather, vec, a, s);
-    return update_t<float, false>(gather, vec, a, s);
+    if (dtype == 0) return master ? update_t<uint16_t, true>(addr, vec, a, s) : update_t<uint16_t, false>(addr, vec, a, s);
+    return update_t<float, false>(addr, vec, a, s);
 }
 
-hipError_t launch_update_step(int dtype, bool gather, const StepArgs& a, hipStream_t s)
+hipError_t launch_update_step(int dtype, int addr, const StepArgs& a, hipStream_t s)
 {
-    const int64_t waves_needed = a.tile_begin[a.K];
-    const int64_t blocks = grid_for(waves_needed * 64);
-    if (dtype == 0) {
-        if (gather) hipLaunchKernelGGL((k_update_step<uint16_t, true>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a);
-        else hipLaunchKernelGGL((k_update_step<uint16_t, false>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a);
-    } else {
-        if (gather) hipLaunchKernelGGL((k_update_step<float, true>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a);
-        else hipLaunchKernelGGL((k_update_step<float, false>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a);
-    }
-    return hipGetLastError();
+    return dtype == 0 ? update_step_t<uint16_t>(addr, a, s) : update_step_t<float>(addr, a, s);
 }
 
 hipError_t launch_normalize(const NormalizeArgs& a, hipStream_t s)

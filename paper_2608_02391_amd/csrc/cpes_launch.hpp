@@ -10,17 +10,21 @@ namespace cpes {
 constexpr int kBlock = 256;             // threads per workgroup for streaming kernels
 constexpr int64_t kMaxGrid = 1 << 20;   // workgroups per launch; larger jobs loop
 
-// One subspace operation: positions j in [0, length) at parameter offset + j
-// or index[offset + j].
+// Subspace addressing modes (see cpes_subspace).
+enum AddrMode { kAddrContig = 0, kAddrGather = 1, kAddrChunk = 2 };
+
+// One subspace operation: positions j in [0, length) at parameter offset + j,
+// index[offset + j], or index[offset + j / 2^s] * 2^s + j mod 2^s (chunks).
 struct StreamArgs {
     void* w;
     const int64_t* index;   // null: contiguous
-    void* aux;              // snapshot (dtype of w) or fp32 master, may be null
+    void* aux;              // snapshot / backup (dtype of w) or fp32 master, may be null
     int64_t offset;
     int64_t length;
     int64_t numel;
     uint32_t k0, k1;        // Philox key = member seed
     float scale;            // +-sigma applied to the noise
+    int32_t chunk_shift;    // s for chunked subspaces
 };
 
 enum AuxKind { kAuxNone = 0, kAuxSnapshot = 1, kAuxMaster = 2, kAuxBackup = 3 };
@@ -40,6 +44,7 @@ struct UpdateArgs {
     float step;
     int32_t n_members;
     int32_t n_streams;
+    int32_t chunk_shift;
     uint32_t seed_lo[kMaxMembers];
     uint32_t seed_hi[kMaxMembers];
     uint8_t member_stream[kMaxMembers];
@@ -59,8 +64,10 @@ struct StepArgs {
     int32_t K;
     int32_t n_members;
     int32_t n_streams;
+    int32_t chunk_shift;
     uint32_t vec_mask;                             // bit k: subspace k takes 16-byte vectors
-    int64_t offset[kMaxStepSubspaces + 1];         // subspace k = positions [offset[k], offset[k+1])
+    int64_t offset[kMaxStepSubspaces + 1];         // subspace k starts at position / map entry offset[k]
+    int64_t length[kMaxStepSubspaces];             // and has length[k] positions
     int64_t tile_begin[kMaxStepSubspaces + 1];     // first wave tile of subspace k
     int32_t stream_begin[kMaxStepSubspaces + 1];   // streams of subspace k
     float step[kMaxStepSubspaces];
@@ -100,12 +107,12 @@ constexpr int kTileItems = 32;
 constexpr int64_t kTile = 64 * kTileItems;
 constexpr int kScanChunk = 4096;        // scan entries per workgroup
 
-hipError_t launch_perturb(int dtype, int aux, bool gather, bool vec, const StreamArgs& a, hipStream_t s);
-hipError_t launch_restore_copy(int dtype, bool gather, bool vec, const StreamArgs& a, hipStream_t s);
-hipError_t launch_restore_master(bool gather, bool vec, const StreamArgs& a, hipStream_t s);
-hipError_t launch_stage_master(int dtype, bool gather, bool vec, const StreamArgs& a, hipStream_t s);
-hipError_t launch_update(int dtype, bool master, bool gather, bool vec, const UpdateArgs& a, hipStream_t s);
-hipError_t launch_update_step(int dtype, bool gather, const StepArgs& a, hipStream_t s);
+hipError_t launch_perturb(int dtype, int aux, int addr, bool vec, const StreamArgs& a, hipStream_t s);
+hipError_t launch_restore_copy(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s);
+hipError_t launch_restore_master(int addr, bool vec, const StreamArgs& a, hipStream_t s);
+hipError_t launch_stage_master(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s);
+hipError_t launch_update(int dtype, bool master, int addr, bool vec, const UpdateArgs& a, hipStream_t s);
+hipError_t launch_update_step(int dtype, int addr, const StepArgs& a, hipStream_t s);
 hipError_t launch_normalize(const NormalizeArgs& a, hipStream_t s);
 hipError_t launch_partition(const PartitionArgs& a, hipStream_t s);
 hipError_t launch_debug_philox(uint64_t seed, uint32_t domain, uint64_t q0, int64_t nblocks,

@@ -37,7 +37,7 @@ def test_header_declares_the_boundary():
 def test_library_exports_every_declared_symbol(lib):
     for name in _declared():
         assert hasattr(lib, name), name
-    assert lib.cpes_abi_version() == 1
+    assert lib.cpes_abi_version() == 2
 
 
 def _sub(offset=0, length=16, index=None):
@@ -176,8 +176,8 @@ def test_update_step_rejects_bad_arguments(lib):
     dec = (ctypes.c_int64 * 3)(0, 40, 32)
     def call(**kw):
         return lib.cpes_update_step(kw.get("w", FAKE), kw.get("numel", 64), cp.BF16, kw.get("K", 2), kw.get("off", off),
-                                    None, 4, seeds, signs, kw.get("subs", subs), FAKE, 5e-4, kw.get("sig", sig),
-                                    kw.get("scale", 0), None)
+                                    kw.get("index", None), kw.get("chunk", 0), kw.get("lens", None), 4, seeds, signs,
+                                    kw.get("subs", subs), FAKE, 5e-4, kw.get("sig", sig), kw.get("scale", 0), None)
     assert call(w=None) == cp.ERR_INVALID_ARGUMENT
     assert call(K=0) == cp.ERR_INVALID_ARGUMENT
     assert call(K=40) == cp.ERR_UNSUPPORTED
@@ -185,4 +185,24 @@ def test_update_step_rejects_bad_arguments(lib):
     assert call(sig=zero_sig) == cp.ERR_INVALID_ARGUMENT
     assert call(off=dec) == cp.ERR_INVALID_ARGUMENT
     assert call(numel=63) == cp.ERR_INVALID_ARGUMENT
+    assert call(index=FAKE, chunk=64, lens=None) == cp.ERR_INVALID_ARGUMENT          # chunked needs lengths
+    assert call(index=FAKE, chunk=24, lens=(ctypes.c_int64 * 2)(8, 8)) == cp.ERR_INVALID_ARGUMENT
+    assert call(index=FAKE, chunk=8, lens=(ctypes.c_int64 * 2)(257, 8)) == cp.ERR_INVALID_ARGUMENT  # > 32 chunks x 8
     assert lib.cpes_last_error().decode().startswith("cpes_update_step")
+
+
+def test_chunked_subspaces_are_validated(lib):
+    for chunk, index in ((12, FAKE), (4, FAKE), (1 << 31, FAKE), (64, None)):
+        s = cp.Subspace(0, 16, index, chunk)
+        assert lib.cpes_perturb(FAKE, 64, cp.BF16, ctypes.byref(s), 1e-3, 1, 1, None, cp.AUX_NONE, None) == \
+            cp.ERR_INVALID_ARGUMENT, chunk
+    offs = (ctypes.c_int64 * 4)()
+    lens = (ctypes.c_int64 * 3)()
+    assert lib.cpes_partition_chunks(1000, 24, 3, 0, offs, lens, FAKE, FAKE, 1 << 20, None, None) == \
+        cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_partition_chunks(1000, 512, 3, 0, offs, lens, FAKE, FAKE, 1 << 20, None, None) == \
+        cp.ERR_INVALID_ARGUMENT                                                       # 2 chunks < K
+    need = lib.cpes_partition_chunks_workspace_bytes(1 << 20, 64, 3)
+    assert need > 0 and lib.cpes_partition_chunks_workspace_bytes(1 << 20, 48, 3) == 0
+    assert lib.cpes_partition_chunks(1 << 20, 64, 3, 0, offs, lens, FAKE, FAKE, need - 1, None, None) == \
+        cp.ERR_WORKSPACE

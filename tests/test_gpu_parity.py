@@ -96,7 +96,8 @@ def test_gpu_normal_statistics(T):
 
 # ------------------------------------------------------------ perturb etc --
 
-LAYOUTS = ["aligned", "unaligned", "gather"]
+LAYOUTS = ["aligned", "unaligned", "gather", "chunked"]
+CHUNK = 64
 LENGTHS = [1, 7, 9, 4095, (1 << 20) + 5]
 
 
@@ -105,6 +106,13 @@ def _perm_partition(d):
     import oracle as O
 
     return O.partition(O.PART_PERMUTATION, d, 4, seed=33)
+
+
+@functools.lru_cache(maxsize=None)
+def _chunk_partition(d):
+    import oracle as O
+
+    return O.partition_chunks(d, CHUNK, 4, 33)
 
 
 def _layout(layout, length):
@@ -123,9 +131,21 @@ def _layout(layout, length):
 
 
 def _setup(orc, T, dtype, layout, length, wseed):
+    """Host weights, device weights, host (offset, element map) for the oracle,
+    and the device subspace.  A chunked subspace is subspace 1 of a 4-way
+    chunk partition (chunk 64): the device gets its chunk list, the oracle the
+    element map the chunk list expands to."""
+    if layout == "chunked":
+        d = 4 * (length + 2 * CHUNK)
+        offs, lens, chunks = _chunk_partition(d)
+        assert lens[1] >= length
+        w = S.host_weights(d, dtype, wseed)
+        index = orc.expand_chunks(chunks, int(offs[1]), length, CHUNK)
+        sub = cp.subspace(int(offs[1]), length, to_dev(chunks), CHUNK)
+        return w, to_dev(w), 0, index, sub
     numel, offset, index = _layout(layout, length)
     w = S.host_weights(numel, dtype, wseed)
-    return w, to_dev(w), offset, index, (to_dev(index) if index is not None else None)
+    return w, to_dev(w), offset, index, cp.subspace(offset, length, to_dev(index) if index is not None else None)
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
@@ -133,7 +153,7 @@ def _setup(orc, T, dtype, layout, length, wseed):
 @pytest.mark.parametrize("dtype,aux", [(S.BF16, 0), (S.BF16, 1), (S.BF16, 2), (S.BF16, 3), (S.F32, 0), (S.F32, 1),
                                        (S.F32, 3)])
 def test_perturb_matches_oracle(orc, T, dtype, aux, layout, length):
-    w, dw, off, index, dindex = _setup(orc, T, dtype, layout, length, 1000 + length)
+    w, dw, off, index, s = _setup(orc, T, dtype, layout, length, 1000 + length)
     sigma, seed, sign = np.float32(2.8284e-3), 17 + length, (-1 if length % 2 else 1)
     w0 = w.copy()
     snap_h = snap_d = master_h = master_d = None
@@ -146,7 +166,6 @@ def test_perturb_matches_oracle(orc, T, dtype, aux, layout, length):
     if aux == 3:                                                      # an existing backup (other values)
         master_h = S.host_weights(length, dtype, 9 + length)
         master_d = to_dev(master_h)
-    s = cp.subspace(off, length, dindex)
     cp.cpes_perturb(dw, s, float(sigma), seed, sign, aux=snap_d if aux == 1 else master_d, aux_mode=aux)
     orc.perturb(w, off, length, sigma, seed, sign, index=index, aux=snap_h if aux == 1 else master_h, aux_mode=aux)
     _sync(T)
@@ -154,6 +173,7 @@ def test_perturb_matches_oracle(orc, T, dtype, aux, layout, length):
     touched = np.zeros(w.size, dtype=bool)
     pos = index[off:off + length] if index is not None else np.arange(off, off + length)
     touched[pos] = True
+    assert np.unique(pos).size == length
     assert np.array_equal(got[~touched], w0[~touched])              # outside: bitwise untouched
     if dtype == S.BF16:
         assert ulp_bf16(got[touched], w[touched]).max() <= 1
@@ -168,8 +188,7 @@ def test_perturb_matches_oracle(orc, T, dtype, aux, layout, length):
 @pytest.mark.parametrize("dtype", [S.BF16, S.F32])
 def test_snapshot_and_master_restore_are_identities(orc, T, dtype, layout):
     length = (1 << 20) + 5
-    w, dw, off, index, dindex = _setup(orc, T, dtype, layout, length, 5)
-    s = cp.subspace(off, length, dindex)
+    w, dw, off, index, s = _setup(orc, T, dtype, layout, length, 5)
     snap = T.empty(length, dtype=dw.dtype, device="cuda")
     cp.cpes_perturb(dw, s, 4e-3, 99, 1, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
     _sync(T)
@@ -193,8 +212,7 @@ def test_snapshot_and_master_restore_are_identities(orc, T, dtype, layout):
 @pytest.mark.parametrize("dtype", [S.BF16, S.F32])
 def test_replay_restore_matches_oracle(orc, T, dtype, layout):
     length = 300007
-    w, dw, off, index, dindex = _setup(orc, T, dtype, layout, length, 6)
-    s = cp.subspace(off, length, dindex)
+    w, dw, off, index, s = _setup(orc, T, dtype, layout, length, 6)
     cp.cpes_perturb(dw, s, 2e-3, 3, -1)
     cp.cpes_restore(dw, s, 2e-3, 3, -1, aux=None, aux_mode=cp.AUX_NONE)
     orc.perturb(w, off, length, np.float32(2e-3), 3, -1, index=index)
@@ -268,12 +286,11 @@ def test_update_matches_oracle(orc, T, kind, layout, members):
     n = len(seeds)
     length = (1 << 18) + 5 if n > 30 else (1 << 20) + 3
     dtype = S.F32 if kind == "f32" else S.BF16
-    w, dw, off, index, dindex = _setup(orc, T, dtype, layout, length, 20 + n)
+    w, dw, off, index, s = _setup(orc, T, dtype, layout, length, 20 + n)
     r = S.rewards("uniform", n, 7 + n)
     rnorm, _ = orc.normalize(r, S.NORM_Z)
     scale = S.SCALE_ALPHA_OVER_N if members == "pairs4" else S.SCALE_ALPHA_OVER_N_SIGMA
     alpha, sigma = np.float32(5e-4), np.float32(2.25e-3)
-    s = cp.subspace(off, length, dindex)
     master_h = master_d = None
     if kind == "master":
         pos = index[off:off + length] if index is not None else np.arange(off, off + length)
@@ -341,6 +358,7 @@ def test_prp_values_bit_exact(orc, T):
 STEP_CASES = {
     # name: (d, K, partition, members per subspace)
     "paper_perm_k4_n40": ((1 << 20) + 3, 4, "perm", [10, 10, 10, 10]),
+    "paper_chunk_k4_n40": ((1 << 20) + 3, 4, "chunk", [10, 10, 10, 10]),
     "contig_unaligned": (300007, 3, [0, 1001, 150003, 300007], [5, 3, 4]),
     "contig_k1_std_es": (262147, 1, "equal", [8]),
     "contig_k8_empty": ((1 << 19) + 64, 8, "equal", [2, 0, 3, 1, 1, 0, 2, 2]),
@@ -352,8 +370,17 @@ STEP_CASES = {
 @pytest.mark.parametrize("scale", [S.SCALE_ALPHA_OVER_N, S.SCALE_ALPHA_OVER_N_SIGMA])
 def test_update_step_matches_oracle(orc, T, case, dtype, scale):
     d, K, part, per = STEP_CASES[case]
-    index = dindex = None
-    if part == "perm":
+    index = dindex = lengths = None
+    chunk = 0
+    if part == "chunk":
+        chunk = 256
+        offsets, lengths, chunks = orc.partition_chunks(d, chunk, K, 33)
+        dindex = to_dev(chunks)
+        # the oracle sees each chunked subspace through its element map, laid end to end
+        maps = [orc.expand_chunks(chunks, int(offsets[k]), int(lengths[k]), chunk) for k in range(K)]
+        index = np.concatenate(maps)
+        host_offsets = np.concatenate([[0], np.cumsum(lengths)])
+    elif part == "perm":
         offsets, index = orc.partition(orc.PART_PERMUTATION, d, K, seed=33)
         dindex = to_dev(index)
     elif part == "equal":
@@ -361,16 +388,20 @@ def test_update_step_matches_oracle(orc, T, case, dtype, scale):
     else:
         offsets = np.array(part, dtype=np.int64)
     offsets = [int(x) for x in offsets]
+    if part != "chunk":
+        host_offsets = offsets
     subs = [k for k in range(K) for _ in range(per[k])]
     n = len(subs)
     seeds = [1 + i for i in range(n)]
     signs = [1 if i % 3 else -1 for i in range(n)]
     rhat, _ = orc.normalize(S.rewards("uniform", n, 99), S.NORM_Z)        # joint standardisation (Eq. 12)
-    sigmas = [float(np.float32(1e-3 * np.sqrt(d / max(1, offsets[k + 1] - offsets[k])))) for k in range(K)]
+    sigmas = [float(np.float32(1e-3 * np.sqrt(d / max(1, host_offsets[k + 1] - host_offsets[k])))) for k in range(K)]
     w = S.host_weights(d, dtype, 70)
     dw = to_dev(w)
-    cp.cpes_update_step(dw, offsets, seeds, signs, subs, to_dev(rhat), 5e-4, sigmas, scale, index=dindex)
-    orc.update_step(w, offsets, seeds, signs, subs, rhat, np.float32(5e-4), np.float32(sigmas), scale, index=index)
+    cp.cpes_update_step(dw, offsets, seeds, signs, subs, to_dev(rhat), 5e-4, sigmas, scale, index=dindex, chunk=chunk,
+                        lengths=lengths)
+    orc.update_step(w, host_offsets, seeds, signs, subs, rhat, np.float32(5e-4), np.float32(sigmas), scale,
+                    index=index)
     _sync(T)
     got = to_host(dw)
     if dtype == S.BF16:
@@ -399,3 +430,17 @@ def test_update_step_with_grouped_standardisation(orc, T):
     _sync(T)
     assert np.array_equal(to_host(rn), rhat)
     assert bf16_close(to_host(dw), w)
+
+
+@pytest.mark.parametrize("d,chunk,K", [(1000, 8, 3), ((1 << 20) + 5, 64, 8), (10000003, 4096, 16), (65536, 65536, 1)])
+def test_chunk_partition_bit_exact(orc, T, d, chunk, K):
+    n_chunks = -(-d // chunk)
+    ws = T.empty(cp.cpes_partition_chunks_workspace_bytes(d, chunk, K), dtype=T.uint8, device="cuda")
+    chunks = T.full((n_chunks,), -1, dtype=T.int64, device="cuda")
+    st = T.full((1,), -7, dtype=T.int32, device="cuda")
+    offs, lens = cp.cpes_partition_chunks(d, chunk, K, 33, chunks, ws, status=st)
+    r_offs, r_lens, r_chunks = orc.partition_chunks(d, chunk, K, 33)
+    _sync(T)
+    assert int(st.item()) == 0
+    assert offs == [int(x) for x in r_offs] and lens == [int(x) for x in r_lens]
+    assert np.array_equal(to_host(chunks), r_chunks)

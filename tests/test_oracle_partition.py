@@ -102,3 +102,25 @@ def test_contiguous_partition(orc):
         orc.partition(orc.PART_CONTIGUOUS, 10, 3, bounds=[0, 5, 6, 9])
     with pytest.raises(ValueError):
         orc.partition(orc.PART_CONTIGUOUS, 10, 11)
+
+
+@pytest.mark.parametrize("d,chunk,K", [(1000, 8, 3), ((1 << 16) + 5, 64, 4), (100003, 256, 8), (4096, 4096, 1)])
+def test_chunk_partition_covers_every_parameter_once(orc, d, chunk, K):
+    """Chunk-to-subspace assignment (partition replay at chunk granularity):
+    the chunks of all subspaces cover [0, d) exactly once, the short last chunk
+    counts only its real parameters, and chunk lists are ascending."""
+    offs, lens, chunks = orc.partition_chunks(d, chunk, K, 33)
+    n_chunks = -(-d // chunk)
+    assert list(offs) == [-(-k * n_chunks // K) for k in range(K + 1)]
+    assert lens.sum() == d
+    seen = np.zeros(d, dtype=np.int64)
+    for k in range(K):
+        seg = chunks[offs[k]:offs[k + 1]]
+        assert np.all(np.diff(seg) > 0)
+        m = orc.expand_chunks(chunks, offs[k], lens[k], chunk)
+        assert m.size == lens[k] and np.all(m < d)
+        seen[m] += 1
+    assert np.all(seen == 1)
+    # the chunk assignment is the element partition of the chunk ids
+    o2, idx = orc.partition(orc.PART_PERMUTATION, n_chunks, K, seed=33)
+    assert np.array_equal(o2, offs) and np.array_equal(idx, chunks)
