@@ -47,7 +47,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=3)
     p.add_argument("--warmup", type=int, default=1)
-    p.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5"])
+    p.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c4c", "p0"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--kernels-once", action="store_true",
                    help="run each kernel once on one 504,654,080-position subspace (for counter passes) and exit")
@@ -84,56 +84,88 @@ class KernelTimer:
 
 
 def build_plan(W, cp, torch):
-    """Device buffers and the per-step call sequence of workload W."""
+    """Device buffers of workload W (weights, maps, backup, rewards)."""
     import numpy as np
 
     import synthetic as S
 
     dev = torch.device("cuda")
     w = S.device_weights(W.d, W.dtype, W.weight_seed)
-    sizes = W.sizes()
     index = ws = None
     if W.partition_mode == S.PART_PERMUTATION:
         index = torch.empty(W.d, dtype=torch.int64, device=dev)
         ws = torch.empty(cp.cpes_partition_workspace_bytes(cp.PART_PERMUTATION, W.d, W.K), dtype=torch.uint8,
                          device=dev)
-    maxk = max(sizes[k] for k in W.active)
+    elif W.partition_mode == S.PART_CHUNKED:
+        index = torch.empty(-(-W.d // W.chunk), dtype=torch.int64, device=dev)
+        ws = torch.empty(cp.cpes_partition_chunks_workspace_bytes(W.d, W.chunk, W.K), dtype=torch.uint8, device=dev)
+    maxk = max(W.sizes()) + 2 * W.chunk        # a chunked subspace exceeds d/K by under two chunks
     tdt = torch.bfloat16 if W.dtype == S.BF16 else torch.float32
     aux = torch.empty(maxk, dtype=torch.float32 if W.master else tdt, device=dev)
-    n_iter = len(W.active)
+    n_iter = 1 if W.copes_step else len(W.active)
     rewards = torch.from_numpy(np.stack([W.rewards(t) for t in range(n_iter)])).to(dev)
     rnorm = torch.empty_like(rewards)
-    return dict(w=w, index=index, ws=ws, aux=aux, rewards=rewards, rnorm=rnorm, sizes=sizes)
+    return dict(w=w, index=index, ws=ws, aux=aux, rewards=rewards, rnorm=rnorm)
 
 
-def run_step(W, cp, torch, P, timer, offsets_cache):
+def random_partition(W, cp, P):
+    """Permutation or chunk partition into P (done once, timed on its own):
+    list of (offset, length) per subspace."""
     import synthetic as S
 
     if W.partition_mode == S.PART_PERMUTATION:
-        if "perm" not in offsets_cache:   # partition is timed on its own (a one-off per ES step)
-            offsets_cache["perm"] = cp.cpes_partition(cp.PART_PERMUTATION, W.d, W.K, W.partition_seed,
-                                                      index=P["index"], workspace=P["ws"])
-        offsets = offsets_cache["perm"]
+        offs = cp.cpes_partition(cp.PART_PERMUTATION, W.d, W.K, W.partition_seed, index=P["index"], workspace=P["ws"])
+        return [(offs[k], offs[k + 1] - offs[k]) for k in range(W.K)]
+    offs, lens = cp.cpes_partition_chunks(W.d, W.chunk, W.K, W.partition_seed, P["index"], P["ws"])
+    P["chunk_offsets"], P["chunk_lengths"] = offs, lens
+    return [(offs[k], lens[k]) for k in range(W.K)]
+
+
+def run_step(W, cp, torch, P, timer, cache):
+    """One pass of the hot path over the workload."""
+    import synthetic as S
+
+    if W.partition_mode == S.PART_CONTIGUOUS:
+        offs = cp.cpes_partition(cp.PART_CONTIGUOUS, W.d, W.K, bounds=W.bounds)
+        parts = [(offs[k], offs[k + 1] - offs[k]) for k in range(W.K)]
     else:
-        offsets = cp.cpes_partition(cp.PART_CONTIGUOUS, W.d, W.K, bounds=W.bounds)
+        parts = cache["parts"]
+    subs = [cp.subspace(o, n, P["index"], W.chunk) for o, n in parts]
+    sigmas = [float(__import__("numpy").float32(W.sigma * (W.d / n) ** 0.5)) for _, n in parts]
     aux_mode = cp.AUX_MASTER if W.master else cp.AUX_SNAPSHOT
-    for t, k in enumerate(W.active):
-        length = offsets[k + 1] - offsets[k]
-        s = cp.subspace(offsets[k], length, P["index"])
-        sigma = W.sigma_k(k)
-        seeds = W.member_seeds(t)
-        aux = P["aux"][:length]
+
+    def members(k, seeds, signs):
+        s, aux = subs[k], P["aux"][:parts[k][1]]
         if W.master:
             timer.run("stage_master", lambda: cp.cpes_stage_master(P["w"], s, aux))
-        for m, (seed, sign) in enumerate(zip(seeds, W.signs)):
+        for m, (seed, sign) in enumerate(zip(seeds, signs)):
             # the first member takes the backup of the subspace; the others perturb from it
             mode = aux_mode if (W.master or m == 0) else cp.AUX_BACKUP
-            timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigma, seed, sign, aux=aux, aux_mode=mode))
+            timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigmas[k], seed, sign, aux=aux, aux_mode=mode))
             # (the perturbed model would be evaluated here)
             timer.run("restore", lambda: cp.cpes_restore(P["w"], s, aux=aux, aux_mode=aux_mode))
+
+    if W.copes_step:
+        # Alg. 1: every subspace gets N/K members, joint standardisation, one composed update
+        seeds, ks = W.member_seeds(0), W.member_subspaces()
+        for k in W.active:
+            idx = [i for i in range(W.n) if ks[i] == k]
+            members(k, [seeds[i] for i in idx], [W.signs[i] for i in idx])
+        timer.run("normalize", lambda: cp.cpes_normalize_rewards(P["rewards"][0], P["rnorm"][0], W.norm_mode))
+        offsets = [o for o, _ in parts] + [parts[-1][0] + (parts[-1][1] if not W.chunk else 0)]
+        if W.chunk:
+            offsets = P["chunk_offsets"]
+        timer.run("update", lambda: cp.cpes_update_step(
+            P["w"], offsets, seeds, W.signs, ks, P["rnorm"][0], W.alpha, sigmas, W.scale_mode,
+            index=P["index"], chunk=W.chunk, lengths=[n for _, n in parts] if W.chunk else None))
+        return
+    for t, k in enumerate(W.active):
+        seeds = W.member_seeds(t)
+        members(k, seeds, W.signs)
         timer.run("normalize", lambda: cp.cpes_normalize_rewards(P["rewards"][t], P["rnorm"][t], W.norm_mode))
-        timer.run("update", lambda: cp.cpes_update(P["w"], s, seeds, W.signs, P["rnorm"][t], W.alpha, sigma,
-                                                   W.scale_mode, master=aux if W.master else None))
+        timer.run("update", lambda: cp.cpes_update(P["w"], subs[k], seeds, W.signs, P["rnorm"][t], W.alpha,
+                                                   sigmas[k], W.scale_mode,
+                                                   master=P["aux"][:parts[k][1]] if W.master else None))
 
 
 def bytes_per_position(W, op):
@@ -142,10 +174,11 @@ def bytes_per_position(W, op):
 
     e = 2 if W.dtype == S.BF16 else 4
     ix = 8 if W.partition_mode == S.PART_PERMUTATION else 0
+    m = W.n // W.K if W.copes_step else W.n          # members perturbing one subspace
     if op == "perturb":
         # master: read master, write w; else the first member reads w and writes w and the
         # backup, the others read the backup and write w
-        return (4 + e if W.master else (3 * e + (W.n - 1) * 2 * e) / W.n) + ix
+        return (4 + e if W.master else (3 * e + (m - 1) * 2 * e) / m) + ix
     if op == "restore":
         return (4 + e if W.master else 2 * e) + ix
     if op == "update":
@@ -170,26 +203,32 @@ def cpu_baseline(W, positions):
     for t, k in enumerate(W.active[:2]):
         n = min(positions, sizes[k])
         w = S.host_weights(n, W.dtype, 1 + k)
-        seeds = W.member_seeds(t)
+        seeds, signs = W.member_seeds(0 if W.copes_step else t), W.signs
+        if W.copes_step:                                 # this subspace's members only
+            ks = W.member_subspaces()
+            seeds = [x for x, kk in zip(seeds, ks) if kk == k]
+            signs = [x for x, kk in zip(signs, ks) if kk == k]
         aux = np.empty(n, dtype=np.float32 if W.master else w.dtype)
         mode = O.AUX_MASTER if W.master else O.AUX_SNAPSHOT
-        rn, _ = O.normalize(W.rewards(t), W.norm_mode)
+        rn, _ = O.normalize(W.rewards(0 if W.copes_step else t), W.norm_mode)
+        if W.copes_step:
+            rn = rn[[i for i, kk in enumerate(W.member_subspaces()) if kk == k]]
         t0 = time.perf_counter()
         if W.master:
             aux[:] = O.stage_master(w, 0, n)
-        for m, (seed, sign) in enumerate(zip(seeds, W.signs)):
+        for m, (seed, sign) in enumerate(zip(seeds, signs)):
             pmode = mode if (W.master or m == 0) else O.AUX_BACKUP
             O.perturb(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=pmode)
             O.restore(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=mode)
-        O.normalize(W.rewards(t), W.norm_mode)
-        O.update(w, 0, n, seeds, W.signs, rn, np.float32(W.alpha), np.float32(W.sigma_k(k)), W.scale_mode,
+        O.normalize(W.rewards(0 if W.copes_step else t), W.norm_mode)
+        O.update(w, 0, n, seeds, signs, rn, np.float32(W.alpha), np.float32(W.sigma_k(k)), W.scale_mode,
                  master=aux if W.master else None)
         t_total += time.perf_counter() - t0
         pos_total += n
     full_total = sum(sizes[k] for k in W.active)
     step_s = t_total / pos_total * full_total
     return {"value": W.d / step_s, "unit": "params/s", "cores": O.num_threads(), "kind": "oracle",
-            "sample": f"first {positions} positions of subspaces {list(W.active[:2])}, all {W.n} members "
+            "sample": f"first {positions} positions of subspaces {list(W.active[:2])}, all their members "
                       f"(perturb+backup, restore) + normalise + update; {t_total:.1f} s, "
                       f"extrapolated per position to the full step"}
 
@@ -252,11 +291,10 @@ def main():
     torch.cuda.synchronize()
     cache = {}
     part_ms = None
-    if W.partition_mode == S.PART_PERMUTATION:
+    if W.partition_mode != S.PART_CONTIGUOUS:
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        cache["perm"] = cp.cpes_partition(cp.PART_PERMUTATION, W.d, W.K, W.partition_seed, index=P["index"],
-                                          workspace=P["ws"])
+        cache["parts"] = random_partition(W, cp, P)
         e1.record()
         torch.cuda.synchronize()
         part_ms = e0.elapsed_time(e1)
@@ -273,14 +311,15 @@ def main():
     timer.collect()
     ms_step = elapsed * 1e3 / args.steps
 
-    sizes = W.sizes()
+    sizes = [n for _, n in cache["parts"]] if "parts" in cache else W.sizes()
     span = sum(sizes[k] for k in W.active)                # subspace positions visited per step
+    per_sub_members = W.n // W.K if W.copes_step else W.n
     ops = {}
     for op in ("perturb", "restore", "update", "normalize", "stage_master"):
         avg_ms, count, tot_ms = timer.stats(op)
         if count == 0:
             continue
-        per_step = span * (W.n if op in ("perturb", "restore") else 1)
+        per_step = span * (per_sub_members if op in ("perturb", "restore") else 1)
         per_launch = per_step / (count / args.steps)     # average positions per launch
         entry = {"launches": count, "avg_ms": round(avg_ms, 4), "ms_per_step": round(tot_ms / args.steps, 3),
                  "positions_per_launch": round(per_launch)}
@@ -290,13 +329,15 @@ def main():
             entry["GB/s"] = round(gbps, 1)
             entry["frac_hbm"] = round(gbps / HBM_PEAK_GBPS, 4)
         if op in ("perturb", "update"):
-            streams = len(set(W.member_seeds(0))) if op == "update" else 1
+            streams = 1
+            if op == "update":
+                streams = len(set(W.member_seeds(0))) // (W.K if W.copes_step else 1)
             entry["params/s"] = round(per_launch / (avg_ms * 1e-3), 1)
             entry["Gnormal/s"] = round(streams * per_launch / (avg_ms * 1e-3) / 1e9, 2)
         ops[op] = entry
     dominant = max((o for o in ops if o != "normalize"), key=lambda o: ops[o]["ms_per_step"])
     d_entry = ops[dominant]
-    gather = W.partition_mode == S.PART_PERMUTATION
+    gather = W.partition_mode != S.PART_CONTIGUOUS
     key = dominant + ("_master" if W.master and dominant in ("perturb", "update", "restore") else "")
     meas = None if (gather or W.dtype != S.BF16) else MEASURED.get(key)
     traffic = None

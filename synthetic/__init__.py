@@ -24,6 +24,12 @@ Workloads (weights N(0, 0.02); sigma = 1e-3; alpha = 5e-4 unless stated):
 * ``c5`` -- the c3 buffer with an fp32 master of the active subspace; 16 equal
   contiguous subspaces visited round-robin over 16 iterations; 128 members =
   64 seeds x (+, -) per iteration; rewards = mean of 8 Bernoulli(0.4) draws.
+* ``c4c`` -- c4 with a chunk-granular permutation (chunks of 65,536
+  parameters, seed 33) instead of an element-level one.
+* ``p0`` -- one CoPES step as the paper runs it (Alg. 1, Table S2): the c3
+  buffer, K = 4 chunk-granular random subspaces (chunks of 65,536), N = 40
+  members split 10 per subspace, rewards U[0,1) standardised jointly (Eq. 12),
+  update alpha / N_k (Eq. 13) over all subspaces in one call.
 
 The effective perturbation scale passed to the library is
 sigma_k = sigma * sqrt(d / d_k) (the dimension-aware scale of Eq. 11).
@@ -37,7 +43,7 @@ from typing import List, Optional, Sequence, Tuple
 import numpy as np
 
 BF16, F32 = 0, 1
-PART_CONTIGUOUS, PART_PERMUTATION = 0, 1
+PART_CONTIGUOUS, PART_PERMUTATION, PART_CHUNKED = 0, 1, 2
 NORM_Z, NORM_RANK = 0, 1
 SCALE_ALPHA_OVER_N_SIGMA, SCALE_ALPHA_OVER_N = 0, 1
 
@@ -155,6 +161,8 @@ class Workload:
     weight_seed: int = 0
     active: Sequence[int] = (0,)          # subspaces visited, in order
     seed_stride: int = 0                  # member seeds of iteration t are seeds + t * seed_stride
+    chunk: int = 0                        # chunk size of a chunk-granular partition
+    copes_step: bool = False              # members split across all subspaces, one joint update
     description: str = ""
 
     @property
@@ -162,9 +170,15 @@ class Workload:
         return len(self.seeds)
 
     def sizes(self) -> List[int]:
+        """Nominal subspace sizes (chunked partitions: K equal shares of d)."""
         if self.bounds is not None:
             return [self.bounds[k + 1] - self.bounds[k] for k in range(self.K)]
         return [-(-(k + 1) * self.d // self.K) - (-(-k * self.d // self.K)) for k in range(self.K)]
+
+    def member_subspaces(self) -> List[int]:
+        """Subspace of each member for a whole CoPES step (N / K per subspace)."""
+        per = self.n // self.K
+        return [i // per for i in range(self.n)]
 
     def sigma_k(self, k: int) -> float:
         """Dimension-aware scale sigma * sqrt(d / d_k) (Eq. 11)."""
@@ -216,7 +230,18 @@ def workload(name: str) -> Workload:
                         "mean_bernoulli", 99, NORM_Z, master=True, active=tuple(range(16)),
                         seed_stride=1000,
                         description="bf16 4,022,468,096 + fp32 master; K=16 round-robin; N=128 antithetic")
+    if name == "c4c":
+        return Workload("c4c", d4, BF16, 8, PART_CHUNKED, None, 33,
+                        list(range(1, 31)), [1] * 30, "uniform", 99, NORM_Z,
+                        active=tuple(range(8)), chunk=1 << 16,
+                        description="bf16 4,022,468,096; 8 chunk-permuted subspaces (chunks of 65,536, seed 33); N=30")
+    if name == "p0":
+        return Workload("p0", d4, BF16, 4, PART_CHUNKED, None, 33,
+                        list(range(1, 41)), [1] * 40, "uniform", 99, NORM_Z,
+                        scale_mode=SCALE_ALPHA_OVER_N, active=tuple(range(4)), chunk=1 << 16, copes_step=True,
+                        description="bf16 4,022,468,096; one CoPES step: K=4 chunk-permuted subspaces, "
+                                    "N=40 (10 per subspace), joint z-score, alpha/N_k")
     raise ValueError(name)
 
 
-WORKLOADS = ("c1", "c2", "c3", "c4", "c5")
+WORKLOADS = ("c1", "c2", "c3", "c4", "c5", "c4c", "p0")

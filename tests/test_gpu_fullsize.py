@@ -222,3 +222,73 @@ def test_c5_master_iteration(orc, T, big):
         got = _host_bits(w[off + p: off + p + WIN])
         assert bf16_close(got, ref), describe_mismatch(bf16_value(got), bf16_value(ref))
     w.copy_(full_before)
+
+
+def _chunk_positions(chunks, off, p, n, chunk):
+    j = np.arange(p, p + n, dtype=np.int64)
+    return chunks[off + j // chunk] * chunk + j % chunk
+
+
+def test_c4c_chunked_subspaces_and_paper_step(orc, T, big):
+    _, w = big
+    W = S.workload("c4c")
+    d, K, C = W.d, W.K, W.chunk
+    _say("c4c: chunk partition of 4 G parameters (chunks of 65,536)")
+    n_chunks = -(-d // C)
+    chunks = T.empty(n_chunks, dtype=T.int64, device="cuda")
+    ws = T.empty(cp.cpes_partition_chunks_workspace_bytes(d, C, K), dtype=T.uint8, device="cuda")
+    offs, lens = cp.cpes_partition_chunks(d, C, K, W.partition_seed, chunks, ws)
+    r_offs, r_lens, r_chunks = orc.partition_chunks(d, C, K, W.partition_seed)
+    T.cuda.synchronize()
+    assert offs == [int(x) for x in r_offs] and lens == [int(x) for x in r_lens]
+    h_chunks = to_host(chunks)
+    assert np.array_equal(h_chunks, r_chunks)
+    rng = np.random.default_rng(11)
+    k = 2
+    off, L = offs[k], lens[k]
+    sigma = float(np.float32(W.sigma * np.sqrt(d / L)))
+    wins = _windows(L, rng, n_random=4)
+    pos = {p: _chunk_positions(h_chunks, off, p, WIN, C) for p in wins}
+    before = {p: _host_bits(w[T.from_numpy(pos[p]).cuda()]) for p in wins}
+    full_before = w.clone()
+    s = cp.subspace(off, L, chunks, C)
+    snap = T.empty(L, dtype=T.bfloat16, device="cuda")
+    _say("c4c: chunked perturb with backup, from backup, restore")
+    cp.cpes_perturb(w, s, sigma, 21, 1, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+    T.cuda.synchronize()
+    for p in wins:
+        ref = before[p].copy()
+        orc.perturb(ref, 0, WIN, np.float32(sigma), 21, 1, j0=p)
+        assert ulp_bf16(_host_bits(w[T.from_numpy(pos[p]).cuda()]), ref).max() <= 1, p
+    cp.cpes_perturb(w, s, sigma, 22, -1, aux=snap, aux_mode=cp.AUX_BACKUP)
+    cp.cpes_restore(w, s, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+    T.cuda.synchronize()
+    assert T.equal(w, full_before)
+    # one CoPES step as the paper runs it: K = 4, N = 40, joint z-score, alpha / N_k
+    P = S.workload("p0")
+    _say("p0: one step update over 4 chunked subspaces, 40 members")
+    p_chunks = T.empty(-(-d // P.chunk), dtype=T.int64, device="cuda")
+    p_ws = T.empty(cp.cpes_partition_chunks_workspace_bytes(d, P.chunk, P.K), dtype=T.uint8, device="cuda")
+    p_offs, p_lens = cp.cpes_partition_chunks(d, P.chunk, P.K, P.partition_seed, p_chunks, p_ws)
+    T.cuda.synchronize()
+    hp = to_host(p_chunks)
+    seeds, ks = P.member_seeds(0), P.member_subspaces()
+    rhat, _ = orc.normalize(P.rewards(0), P.norm_mode)
+    sigmas = [float(np.float32(P.sigma * np.sqrt(d / p_lens[k]))) for k in range(P.K)]
+    p_pos, p_before = {}, {}
+    for kk in range(P.K):
+        p = int(rng.integers(0, p_lens[kk] - WIN))
+        p_pos[kk] = (p, _chunk_positions(hp, p_offs[kk], p, WIN, P.chunk))
+        p_before[kk] = _host_bits(w[T.from_numpy(p_pos[kk][1]).cuda()])
+    cp.cpes_update_step(w, p_offs, seeds, P.signs, ks, T.from_numpy(rhat).cuda(), P.alpha, sigmas, P.scale_mode,
+                        index=p_chunks, chunk=P.chunk, lengths=p_lens)
+    T.cuda.synchronize()
+    for kk in range(P.K):
+        p, ps = p_pos[kk]
+        sel = [i for i in range(P.n) if ks[i] == kk]
+        ref = p_before[kk].copy()
+        orc.update(ref, 0, WIN, [seeds[i] for i in sel], [P.signs[i] for i in sel], rhat[sel], np.float32(P.alpha),
+                   np.float32(sigmas[kk]), P.scale_mode, j0=p)
+        got = _host_bits(w[T.from_numpy(ps).cuda()])
+        assert bf16_close(got, ref), describe_mismatch(bf16_value(got), bf16_value(ref))
+    w.copy_(full_before)
