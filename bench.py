@@ -47,7 +47,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=3)
     p.add_argument("--warmup", type=int, default=1)
-    p.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c4c", "p0"])
+    p.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c4c", "p0", "c3h", "p0h"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--kernels-once", action="store_true",
                    help="run each kernel once on one 504,654,080-position subspace (for counter passes) and exit")
@@ -105,7 +105,8 @@ def build_plan(W, cp, torch):
     n_iter = 1 if W.copes_step else len(W.active)
     rewards = torch.from_numpy(np.stack([W.rewards(t) for t in range(n_iter)])).to(dev)
     rnorm = torch.empty_like(rewards)
-    return dict(w=w, index=index, ws=ws, aux=aux, rewards=rewards, rnorm=rnorm)
+    host = torch.empty(maxk, dtype=tdt, pin_memory=True) if W.host_backup else None
+    return dict(w=w, index=index, ws=ws, aux=aux, rewards=rewards, rnorm=rnorm, host=host)
 
 
 def random_partition(W, cp, P):
@@ -136,6 +137,15 @@ def run_step(W, cp, torch, P, timer, cache):
 
     def members(k, seeds, signs):
         s, aux = subs[k], P["aux"][:parts[k][1]]
+        if W.host_backup:
+            # Sec. 3.3: the pre-perturbation weights go to host memory once, every
+            # member is perturbed in place and restored from there
+            host = P["host"][:parts[k][1]]
+            timer.run("backup_host", lambda: cp.cpes_backup_to_host(P["w"], s, host))
+            for seed, sign in zip(seeds, signs):
+                timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigmas[k], seed, sign))
+                timer.run("restore_host", lambda: cp.cpes_restore_from_host(P["w"], s, host))
+            return
         if W.master:
             timer.run("stage_master", lambda: cp.cpes_stage_master(P["w"], s, aux))
         for m, (seed, sign) in enumerate(zip(seeds, signs)):
@@ -175,6 +185,10 @@ def bytes_per_position(W, op):
     e = 2 if W.dtype == S.BF16 else 4
     ix = 8 if W.partition_mode == S.PART_PERMUTATION else 0
     m = W.n // W.K if W.copes_step else W.n          # members perturbing one subspace
+    if op == "perturb" and W.host_backup:
+        return 2 * e + ix
+    if op in ("backup_host", "restore_host"):
+        return e + ix                                  # HBM side; the same e bytes cross the host link
     if op == "perturb":
         # master: read master, write w; else the first member reads w and writes w and the
         # backup, the others read the backup and write w
@@ -315,11 +329,11 @@ def main():
     span = sum(sizes[k] for k in W.active)                # subspace positions visited per step
     per_sub_members = W.n // W.K if W.copes_step else W.n
     ops = {}
-    for op in ("perturb", "restore", "update", "normalize", "stage_master"):
+    for op in ("perturb", "restore", "update", "normalize", "stage_master", "backup_host", "restore_host"):
         avg_ms, count, tot_ms = timer.stats(op)
         if count == 0:
             continue
-        per_step = span * (per_sub_members if op in ("perturb", "restore") else 1)
+        per_step = span * (per_sub_members if op in ("perturb", "restore", "restore_host") else 1)
         per_launch = per_step / (count / args.steps)     # average positions per launch
         entry = {"launches": count, "avg_ms": round(avg_ms, 4), "ms_per_step": round(tot_ms / args.steps, 3),
                  "positions_per_launch": round(per_launch)}
@@ -328,6 +342,9 @@ def main():
             gbps = b * per_launch / (avg_ms * 1e-3) / 1e9
             entry["GB/s"] = round(gbps, 1)
             entry["frac_hbm"] = round(gbps / HBM_PEAK_GBPS, 4)
+        if op in ("backup_host", "restore_host"):
+            e = 2 if W.dtype == S.BF16 else 4
+            entry["host_link_GB/s"] = round(e * per_launch / (avg_ms * 1e-3) / 1e9, 1)
         if op in ("perturb", "update"):
             streams = 1
             if op == "update":
@@ -335,11 +352,13 @@ def main():
             entry["params/s"] = round(per_launch / (avg_ms * 1e-3), 1)
             entry["Gnormal/s"] = round(streams * per_launch / (avg_ms * 1e-3) / 1e9, 2)
         ops[op] = entry
-    dominant = max((o for o in ops if o != "normalize"), key=lambda o: ops[o]["ms_per_step"])
+    # the dominant GPU kernel; host-link transfers are reported in ops
+    dominant = max((o for o in ops if o not in ("normalize", "backup_host", "restore_host")),
+                   key=lambda o: ops[o]["ms_per_step"])
     d_entry = ops[dominant]
     gather = W.partition_mode != S.PART_CONTIGUOUS
     key = dominant + ("_master" if W.master and dominant in ("perturb", "update", "restore") else "")
-    meas = None if (gather or W.dtype != S.BF16) else MEASURED.get(key)
+    meas = None if (gather or W.dtype != S.BF16 or W.host_backup) else MEASURED.get(key)
     traffic = None
     if meas is not None:
         per_pos = meas.get("hbm_bytes")

@@ -191,6 +191,28 @@ CPES_API int cpes_restore(void* w_dev, int64_t numel, int dtype, const cpes_subs
                  uint64_t seed, int32_t sign, const void* aux_dev, int aux_mode, void* stream);
 
 /*
+ * cpes_backup_to_host -- backup_host[j] = w[p(j)] (bit copy), the weight
+ * backup in host memory (Sec. 3.3; Supp. A.8, CPU weight backup): the
+ * pre-perturbation weights of the subspace leave the GPU, so the backup adds
+ * no device-resident copy.
+ * cpes_restore_from_host -- w[p(j)] = backup_host[j] (bit copy), the restore
+ * after each perturbed-model evaluation.
+ *   backup_host: s->length elements of `dtype`, PINNED host memory the device
+ *                can address (hipHostMalloc, or a torch tensor made with
+ *                pin_memory=True); owned by the caller, who keeps it alive and
+ *                unmodified until the work on `stream` has finished.
+ * A contiguous subspace moves as one DMA copy on `stream`; an index-map or
+ * chunked subspace is gathered / scattered by a kernel that reads or writes
+ * the pinned buffer over the host link.  Both are asynchronous on `stream`.
+ * Errors: as cpes_perturb for w and s; backup_host NULL or not pinned host
+ *   memory (pageable, or device memory) -> CPES_ERR_INVALID_ARGUMENT.
+ */
+CPES_API int cpes_backup_to_host(const void* w_dev, int64_t numel, int dtype, const cpes_subspace* s,
+                        void* backup_host, void* stream);
+CPES_API int cpes_restore_from_host(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s,
+                           const void* backup_host, void* stream);
+
+/*
  * cpes_stage_master -- master_dev[j] = fp32 value of w[p(j)] (exact), the fp32
  * master copy of the active subspace kept while its bf16 weights are
  * perturbed and updated.  Errors as cpes_perturb.

@@ -26,7 +26,7 @@ MAX_MEMBERS, MAX_REWARDS, MAX_GROUPS, MAX_PERMUTATION_K, MAX_STEP_SUBSPACES = 25
 EXPORTED = (
     "cpes_partition", "cpes_partition_workspace_bytes", "cpes_partition_chunks",
     "cpes_partition_chunks_workspace_bytes", "cpes_perturb", "cpes_restore",
-    "cpes_stage_master", "cpes_normalize_rewards", "cpes_update", "cpes_update_step", "cpes_debug_philox",
+    "cpes_backup_to_host", "cpes_restore_from_host", "cpes_stage_master", "cpes_normalize_rewards", "cpes_update", "cpes_update_step", "cpes_debug_philox",
     "cpes_debug_normals", "cpes_debug_bm_grid", "cpes_debug_prp", "cpes_rng_probe",
     "cpes_last_error", "cpes_abi_version",
 )
@@ -64,6 +64,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "cpes_partition_chunks_workspace_bytes": [i64, i64, i32],
         "cpes_perturb": [vp, i64, i32, sp, f32, u64, i32, vp, i32, vp],
         "cpes_restore": [vp, i64, i32, sp, f32, u64, i32, vp, i32, vp],
+        "cpes_backup_to_host": [vp, i64, i32, sp, vp, vp],
+        "cpes_restore_from_host": [vp, i64, i32, sp, vp, vp],
         "cpes_stage_master": [vp, i64, i32, sp, vp, vp],
         "cpes_normalize_rewards": [vp, i32, i32, vp, i32, vp, vp, vp],
         "cpes_update": [vp, i64, i32, sp, vp, i32, vp, vp, vp, f32, f32, i32, vp],
@@ -120,6 +122,20 @@ def _dev_ptr(t, what: str) -> Optional[int]:
         raise ValueError(f"{what} must be a GPU tensor")
     if not t.is_contiguous():
         raise ValueError(f"{what} must be contiguous")
+    return t.data_ptr()
+
+
+def _host_ptr(t, w, s: "Subspace", what: str) -> int:
+    """A host backup: a CPU tensor of w's dtype holding at least s.length
+    elements.  Whether it is pinned is checked by the library."""
+    if t.is_cuda:
+        raise ValueError(f"{what} must be a host tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if t.dtype != w.dtype:
+        raise TypeError(f"{what} must have dtype {w.dtype}, not {t.dtype}")
+    if t.numel() < s.length:
+        raise ValueError(f"{what} holds {t.numel()} elements, {s.length} needed")
     return t.data_ptr()
 
 
@@ -186,6 +202,18 @@ def cpes_restore(w, s: Subspace, sigma: float = 0.0, seed: int = 0, sign: int = 
                  aux_mode: int = AUX_SNAPSHOT, stream=None) -> None:
     _check(load().cpes_restore(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s), sigma, seed, sign,
                                _dev_ptr(aux, "aux"), aux_mode, _stream(stream)))
+
+
+def cpes_backup_to_host(w, s: Subspace, backup, stream=None) -> None:
+    """backup[j] = w[p(j)] into a pinned host tensor (``pin_memory=True``)."""
+    _check(load().cpes_backup_to_host(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s),
+                                      _host_ptr(backup, w, s, "backup"), _stream(stream)))
+
+
+def cpes_restore_from_host(w, s: Subspace, backup, stream=None) -> None:
+    """w[p(j)] = backup[j] from a pinned host tensor."""
+    _check(load().cpes_restore_from_host(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s),
+                                         _host_ptr(backup, w, s, "backup"), _stream(stream)))
 
 
 def cpes_stage_master(w, s: Subspace, master, stream=None) -> None:

@@ -190,6 +190,44 @@ PartitionLayout partition_layout(int64_t d, int32_t K)
     return L;
 }
 
+// A host backup must be pinned memory the device can address (hipHostMalloc,
+// torch pin_memory); a kernel touching pageable memory would fault.  Returns
+// the device-side address of the buffer in *dev.
+int check_pinned_host(const void* p, void** dev, const char* fn)
+{
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, p) != hipSuccess || attr.type != hipMemoryTypeHost) {
+        (void)hipGetLastError();
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: the backup is not pinned host memory", fn);
+    }
+    *dev = attr.devicePointer ? attr.devicePointer : const_cast<void*>(p);
+    return CPES_OK;
+}
+
+int host_backup_copy(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, void* host, bool to_host,
+                     void* stream, const char* fn)
+{
+    int rc = check_subspace(w_dev, numel, dtype, s, fn);
+    if (rc) return rc;
+    if (!host) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: backup pointer is null", fn);
+    if (s->length == 0) return CPES_OK;
+    void* host_dev = nullptr;
+    if ((rc = check_pinned_host(host, &host_dev, fn))) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    if (!s->index) {   // contiguous: one DMA transfer over the host link
+        const size_t bytes = (size_t)s->length * elem_size(dtype);
+        char* dev = static_cast<char*>(w_dev) + (size_t)s->offset * elem_size(dtype);
+        const hipError_t e = to_host ? hipMemcpyAsync(host, dev, bytes, hipMemcpyDeviceToHost, st)
+                                     : hipMemcpyAsync(dev, host, bytes, hipMemcpyHostToDevice, st);
+        return hip_status(e, fn);
+    }
+    // index-map or chunked: the copy kernels address the pinned buffer directly
+    const cpes::StreamArgs a = stream_args(w_dev, numel, s, host_dev, 0, 0.0f);
+    const bool vec = vector_ok(w_dev, dtype, s, host_dev, false);
+    if (to_host) return hip_status(cpes::launch_backup_copy(dtype, addr_mode(s), vec, a, st), fn);
+    return hip_status(cpes::launch_restore_copy(dtype, addr_mode(s), vec, a, st), fn);
+}
+
 }  // namespace
 
 extern "C" {
@@ -353,6 +391,22 @@ int cpes_restore(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, 
     const bool vec = vector_ok(w_dev, dtype, s, aux_dev, aux_mode == CPES_AUX_MASTER);
     if (aux_mode == CPES_AUX_SNAPSHOT) return hip_status(cpes::launch_restore_copy(dtype, addr, vec, a, st), fn);
     return hip_status(cpes::launch_restore_master(addr, vec, a, st), fn);
+}
+
+int cpes_backup_to_host(const void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, void* backup_host,
+                        void* stream)
+{
+    g_error.clear();
+    return host_backup_copy(const_cast<void*>(w_dev), numel, dtype, s, backup_host, true, stream,
+                            "cpes_backup_to_host");
+}
+
+int cpes_restore_from_host(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, const void* backup_host,
+                           void* stream)
+{
+    g_error.clear();
+    return host_backup_copy(w_dev, numel, dtype, s, const_cast<void*>(backup_host), false, stream,
+                            "cpes_restore_from_host");
 }
 
 int cpes_stage_master(const void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float* master_dev,

@@ -263,6 +263,44 @@ __global__ __launch_bounds__(kBlock) void k_restore_copy(StreamArgs a)
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
 
+// Backup copy: backup[j] = w[p(j)] (bit copy), for backups taken apart from a
+// perturbation, e.g. into pinned host memory.
+template <typename T, int ADDR, bool VEC>
+__global__ __launch_bounds__(kBlock) void k_backup_copy(StreamArgs a)
+{
+    constexpr int N = UnitOf<T>::n;
+    const T* w = static_cast<const T*>(a.w);
+    T* backup = static_cast<T*>(a.aux);
+    auto scalar_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+            const int64_t j = j0 + e;
+            int64_t i;
+            if (j < a.length) backup[j] = param_of<ADDR>(a, j, i) ? w[i] : T(0);
+        }
+    };
+    auto vec_body = [&](int64_t u) {
+        const int64_t j0 = u * N;
+        T v[N];
+        if (ADDR == kGather) {
+            int64_t idx[N];
+            load_index<N>(a.index + a.offset + j0, idx);
+#pragma unroll
+            for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
+        } else {
+            int64_t base;
+            if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+                scalar_body(u);
+                return;
+            }
+            load_vec<T>(w + base, v);
+        }
+        store_vec<T>(backup + j0, v);
+    };
+    for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
+}
+
 // Master restore (bf16 weights): w[p(j)] = rne_bf16(master[j]).
 template <int ADDR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_restore_master(StreamArgs a)
@@ -888,6 +926,13 @@ hipError_t restore_copy_t(int addr, bool vec, const StreamArgs& a, hipStream_t s
 }
 
 template <typename T>
+hipError_t backup_copy_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
+{
+    const int64_t u = units_of<T>(a.length);
+    CPES_DISPATCH_ADDR_VEC(k_backup_copy, T)
+}
+
+template <typename T>
 hipError_t stage_master_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
     const int64_t u = units_of<T>(a.length);
@@ -934,6 +979,11 @@ hipError_t launch_perturb(int dtype, int aux, int addr, bool vec, const StreamAr
 hipError_t launch_restore_copy(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
     return dtype == 0 ? restore_copy_t<uint16_t>(addr, vec, a, s) : restore_copy_t<float>(addr, vec, a, s);
+}
+
+hipError_t launch_backup_copy(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s)
+{
+    return dtype == 0 ? backup_copy_t<uint16_t>(addr, vec, a, s) : backup_copy_t<float>(addr, vec, a, s);
 }
 
 hipError_t launch_restore_master(int addr, bool vec, const StreamArgs& a, hipStream_t s)

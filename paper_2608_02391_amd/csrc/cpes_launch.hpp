@@ -110,6 +110,7 @@ constexpr int kScanChunk = 4096;        // scan entries per workgroup
 hipError_t launch_perturb(int dtype, int aux, int addr, bool vec, const StreamArgs& a, hipStream_t s);
 hipError_t launch_restore_copy(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s);
 hipError_t launch_restore_master(int addr, bool vec, const StreamArgs& a, hipStream_t s);
+hipError_t launch_backup_copy(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s);
 hipError_t launch_stage_master(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s);
 hipError_t launch_update(int dtype, bool master, int addr, bool vec, const UpdateArgs& a, hipStream_t s);
 hipError_t launch_update_step(int dtype, int addr, const StepArgs& a, hipStream_t s);

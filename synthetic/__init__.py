@@ -163,6 +163,7 @@ class Workload:
     seed_stride: int = 0                  # member seeds of iteration t are seeds + t * seed_stride
     chunk: int = 0                        # chunk size of a chunk-granular partition
     copes_step: bool = False              # members split across all subspaces, one joint update
+    host_backup: bool = False             # weight backup in pinned host memory instead of HBM
     description: str = ""
 
     @property
@@ -241,7 +242,11 @@ def workload(name: str) -> Workload:
                         scale_mode=SCALE_ALPHA_OVER_N, active=tuple(range(4)), chunk=1 << 16, copes_step=True,
                         description="bf16 4,022,468,096; one CoPES step: K=4 chunk-permuted subspaces, "
                                     "N=40 (10 per subspace), joint z-score, alpha/N_k")
+    if name in ("c3h", "p0h"):
+        base = workload(name[:-1])
+        return dataclasses.replace(base, name=name, host_backup=True,
+                                   description=base.description + "; weight backup in pinned host memory")
     raise ValueError(name)
 
 
-WORKLOADS = ("c1", "c2", "c3", "c4", "c5", "c4c", "p0")
+WORKLOADS = ("c1", "c2", "c3", "c4", "c5", "c4c", "p0", "c3h", "p0h")

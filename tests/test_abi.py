@@ -86,6 +86,21 @@ def test_restore_and_stage_reject_bad_arguments(lib):
     assert lib.cpes_stage_master(FAKE, 10, cp.BF16, ctypes.byref(s), FAKE, None) == cp.ERR_INVALID_ARGUMENT
 
 
+def test_host_backup_rejects_bad_arguments(lib):
+    s = _sub()
+    for fn in (lib.cpes_backup_to_host, lib.cpes_restore_from_host):
+        name = fn.__name__
+        for args in [(None, 64, cp.BF16, ctypes.byref(s), FAKE),       # null weights
+                     (FAKE, 64, 7, ctypes.byref(s), FAKE),             # bad dtype
+                     (FAKE, 64, cp.BF16, None, FAKE),                  # null subspace
+                     (FAKE, 8, cp.BF16, ctypes.byref(s), FAKE),        # beyond numel
+                     (FAKE, 64, cp.BF16, ctypes.byref(s), None)]:      # null backup
+            rc, msg = _rc_msg(lib, fn(*args, None))
+            assert rc == cp.ERR_INVALID_ARGUMENT, (name, args)
+            assert msg.startswith(name + ":"), msg
+        assert fn(FAKE, 64, cp.BF16, ctypes.byref(_sub(3, 0)), FAKE, None) == cp.OK   # empty: no-op
+
+
 def test_normalize_rejects_bad_arguments(lib):
     assert lib.cpes_normalize_rewards(None, 8, cp.NORM_Z, None, 1, FAKE, None, None) == cp.ERR_INVALID_ARGUMENT
     assert lib.cpes_normalize_rewards(FAKE, 0, cp.NORM_Z, None, 1, FAKE, None, None) == cp.ERR_INVALID_ARGUMENT

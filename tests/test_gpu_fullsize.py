@@ -292,3 +292,51 @@ def test_c4c_chunked_subspaces_and_paper_step(orc, T, big):
         got = _host_bits(w[T.from_numpy(ps).cuda()])
         assert bf16_close(got, ref), describe_mismatch(bf16_value(got), bf16_value(ref))
     w.copy_(full_before)
+
+
+def test_host_backup_full_size(orc, T, big):
+    """The weight backup in pinned host memory at full subspace sizes: a c3
+    layer group (one DMA copy each way) and a c4c chunked subspace (kernels
+    reading and writing the pinned buffer).  Sampled windows of the backup
+    equal the weights they were taken from; after a perturbation, the restore
+    from host memory returns the whole 4 G buffer to its bits."""
+    W, w = big
+    full_before = w.clone()
+    rng = np.random.default_rng(5)
+    k = 4
+    off, L = W.bounds[k], W.sizes()[k]
+    hb = T.empty(L, dtype=T.bfloat16, pin_memory=True)
+    _say("host backup: c3 layer group, DMA")
+    cp.cpes_backup_to_host(w, cp.subspace(off, L), hb)
+    T.cuda.synchronize()
+    hbits = to_host(hb)
+    for p in _windows(L, rng, n_random=3):
+        assert np.array_equal(hbits[p:p + WIN], _host_bits(w[off + p: off + p + WIN])), p
+    cp.cpes_perturb(w, cp.subspace(off, L), W.sigma_k(k), 31, 1)
+    cp.cpes_restore_from_host(w, cp.subspace(off, L), hb)
+    T.cuda.synchronize()
+    assert T.equal(w, full_before)
+    del hb, hbits
+    C4 = S.workload("c4c")
+    _say("host backup: c4c chunked subspace, zero-copy kernels")
+    chunks = T.empty(-(-C4.d // C4.chunk), dtype=T.int64, device="cuda")
+    ws = T.empty(cp.cpes_partition_chunks_workspace_bytes(C4.d, C4.chunk, C4.K), dtype=T.uint8, device="cuda")
+    offs, lens = cp.cpes_partition_chunks(C4.d, C4.chunk, C4.K, C4.partition_seed, chunks, ws)
+    T.cuda.synchronize()
+    h_chunks = to_host(chunks)
+    k = C4.K - 1                                     # holds the short last chunk or not; either way ragged-safe
+    off, L = offs[k], lens[k]
+    s = cp.subspace(off, L, chunks, C4.chunk)
+    hb = T.empty(L, dtype=T.bfloat16, pin_memory=True)
+    cp.cpes_backup_to_host(w, s, hb)
+    T.cuda.synchronize()
+    hbits = to_host(hb)
+    for p in _windows(L, rng, n_random=3):
+        pos = _chunk_positions(h_chunks, off, p, WIN, C4.chunk)
+        assert np.array_equal(hbits[p:p + WIN], _host_bits(w[T.from_numpy(pos).cuda()])), p
+    cp.cpes_perturb(w, s, float(np.float32(C4.sigma * np.sqrt(C4.d / L))), 32, -1)
+    T.cuda.synchronize()
+    assert not T.equal(w, full_before)
+    cp.cpes_restore_from_host(w, s, hb)
+    T.cuda.synchronize()
+    assert T.equal(w, full_before)

@@ -225,6 +225,73 @@ def test_replay_restore_matches_oracle(orc, T, dtype, layout):
         assert f32_close(got, w)
 
 
+# ------------------------------------------------------ host-memory backup --
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("length", [1, 7, 4095, (1 << 20) + 5])
+@pytest.mark.parametrize("dtype", [S.BF16, S.F32])
+def test_host_backup_round_trip(orc, T, dtype, layout, length):
+    """The backup written to pinned host memory is the oracle's snapshot, bit
+    for bit, and restoring from it undoes a perturbation exactly."""
+    w, dw, off, index, s = _setup(orc, T, dtype, layout, length, 40 + length)
+    w0 = w.copy()
+    hb = T.full((length,), 7, dtype=dw.dtype, pin_memory=True)
+    cp.cpes_backup_to_host(dw, s, hb)
+    snap = np.zeros(length, dtype=w.dtype)
+    orc.perturb(w, off, length, np.float32(3e-3), 8, 1, index=index, aux=snap, aux_mode=orc.AUX_SNAPSHOT)
+    cp.cpes_perturb(dw, s, 3e-3, 8, 1)
+    _sync(T)
+    assert np.array_equal(to_host(hb), snap)
+    got = to_host(dw)
+    if dtype == S.BF16:
+        assert ulp_bf16(got, w).max() <= 1
+    else:
+        assert f32_close(got, w)
+    cp.cpes_restore_from_host(dw, s, hb)
+    orc.restore(w, off, length, 0.0, 0, 1, index=index, aux=snap, aux_mode=orc.AUX_SNAPSHOT)
+    _sync(T)
+    assert np.array_equal(w, w0)
+    assert np.array_equal(to_host(dw), w0)
+
+
+@pytest.mark.parametrize("layout", ["unaligned", "chunked"])
+def test_host_backup_member_loop(orc, T, layout):
+    """One host backup per step, then perturb / restore for every member: each
+    member is perturbed from the same pre-update weights (the oracle perturbs
+    a fresh copy of them), and the weights return to them bit for bit."""
+    length = 300007
+    w, dw, off, index, s = _setup(orc, T, S.BF16, layout, length, 77)
+    hb = T.empty((length,), dtype=dw.dtype, pin_memory=True)
+    cp.cpes_backup_to_host(dw, s, hb)
+    for m, (seed, sign) in enumerate([(11, 1), (11, -1), (12, 1), (13, -1)]):
+        cp.cpes_perturb(dw, s, 2e-3, seed, sign)
+        _sync(T)
+        ref = w.copy()
+        orc.perturb(ref, off, length, np.float32(2e-3), seed, sign, index=index)
+        assert ulp_bf16(to_host(dw), ref).max() <= 1, f"member {m}"
+        cp.cpes_restore_from_host(dw, s, hb)
+    _sync(T)
+    assert np.array_equal(to_host(dw), w)
+
+
+def test_host_backup_rejects_unpinned_and_device_buffers(orc, T):
+    w, dw, off, index, s = _setup(orc, T, S.BF16, "aligned", 4096, 3)
+    pageable = T.empty((4096,), dtype=dw.dtype)
+    assert not pageable.is_pinned()
+    with pytest.raises(cp.CpesError, match="not pinned host memory"):
+        cp.cpes_backup_to_host(dw, s, pageable)
+    with pytest.raises(cp.CpesError, match="not pinned host memory"):
+        cp.cpes_restore_from_host(dw, s, pageable)
+    dev = T.empty((4096,), dtype=dw.dtype, device="cuda")
+    rc = cp.load().cpes_restore_from_host(dw.data_ptr(), dw.numel(), cp.BF16, cp.ctypes.byref(s), dev.data_ptr(),
+                                          None)
+    assert rc == cp.ERR_INVALID_ARGUMENT and "not pinned" in cp.last_error()
+    with pytest.raises(ValueError):
+        cp.cpes_backup_to_host(dw, s, dev)
+    _sync(T)
+    assert np.array_equal(to_host(dw), w)                           # nothing was written
+
+
 # --------------------------------------------------------------- normalise --
 
 @pytest.mark.parametrize("n", [1, 2, 8, 30, 32, 40, 128, 1000, 4096])
