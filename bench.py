@@ -3,8 +3,10 @@
     python bench.py [--steps K] [--warmup W] [--workload c3]
 
 One step = one pass of the hot path over every subspace of the workload:
-for each active subspace: partition lookup, N x (perturb with backup, restore),
-reward normalisation, seed-replayed update.  Inputs (weights, rewards) are
+for each active subspace: partition lookup, N x (perturb, restore from the
+backup), reward normalisation, seed-replayed update.  The first member's
+perturbation also writes the backup; the others perturb the restored weights
+in place.  Inputs (weights, rewards) are
 resident in HBM before the timed region.  Prints ONE JSON line.
 
 Workloads (synthetic, see synthetic/__init__.py): c3 (default; 4,022,468,096
@@ -28,15 +30,15 @@ HBM_PEAK_GBPS = 8000.0                 # MI355X HBM3E
 VALU_LANE_OPS_PEAK = 256 * 64 * 2.4e9  # 256 CUs x 64 lanes x 2.4 GHz: one VALU lane-op per lane per clock
 # Per-kernel figures measured with rocprofv3 on a 504,654,080-position bf16
 # subspace (profiles/c3_subspace_counters.md): VALU instructions per generated
-# normal (SQ_INSTS_VALU / SQ_WAVES / normals per lane) and HBM bytes per
-# position (FETCH_SIZE x 2.0 and WRITE_SIZE x 1.0, the factors a plain copy of
-# known size reads).  Valid for the kernels as profiled; re-measure after a
-# kernel change.
+# normal (SQ_INSTS_VALU x 64 lanes / normals) and HBM bytes per position
+# (FETCH_SIZE x 2.0 and WRITE_SIZE x 1.0, the factors a plain copy of known
+# size reads).  Valid for the kernels as profiled; re-measure after a kernel
+# change.
 MEASURED = {
-    "perturb": {"valu_per_normal": 46.4, "hbm_bytes_first": 6.0, "hbm_bytes_rest": 4.0},
-    "perturb_master": {"valu_per_normal": 44.9, "hbm_bytes": 6.0},
-    "update": {"valu_per_normal": 41.3, "hbm_bytes": 4.0},
-    "update_master": {"valu_per_normal": 41.2, "hbm_bytes": 10.0},
+    "perturb": {"valu_per_normal": 40.0, "hbm_bytes_first": 6.0, "hbm_bytes_rest": 4.0},
+    "perturb_master": {"valu_per_normal": 39.1, "hbm_bytes": 6.0},
+    "update": {"valu_per_normal": 37.5, "hbm_bytes": 4.0},
+    "update_master": {"valu_per_normal": 37.5, "hbm_bytes": 10.0},
     "restore": {"hbm_bytes": 4.0},
     "restore_master": {"hbm_bytes": 6.0},
 }
@@ -149,8 +151,9 @@ def run_step(W, cp, torch, P, timer, cache):
         if W.master:
             timer.run("stage_master", lambda: cp.cpes_stage_master(P["w"], s, aux))
         for m, (seed, sign) in enumerate(zip(seeds, signs)):
-            # the first member takes the backup of the subspace; the others perturb from it
-            mode = aux_mode if (W.master or m == 0) else cp.AUX_BACKUP
+            # the first member takes the backup of the subspace; the others perturb the
+            # restored weights in place (a master source is read by every member)
+            mode = aux_mode if (W.master or m == 0) else cp.AUX_NONE
             timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigmas[k], seed, sign, aux=aux, aux_mode=mode))
             # (the perturbed model would be evaluated here)
             timer.run("restore", lambda: cp.cpes_restore(P["w"], s, aux=aux, aux_mode=aux_mode))
@@ -191,7 +194,7 @@ def bytes_per_position(W, op):
         return e + ix                                  # HBM side; the same e bytes cross the host link
     if op == "perturb":
         # master: read master, write w; else the first member reads w and writes w and the
-        # backup, the others read the backup and write w
+        # backup, the others read and write w
         return (4 + e if W.master else (3 * e + (m - 1) * 2 * e) / m) + ix
     if op == "restore":
         return (4 + e if W.master else 2 * e) + ix
@@ -231,7 +234,7 @@ def cpu_baseline(W, positions):
         if W.master:
             aux[:] = O.stage_master(w, 0, n)
         for m, (seed, sign) in enumerate(zip(seeds, signs)):
-            pmode = mode if (W.master or m == 0) else O.AUX_BACKUP
+            pmode = mode if (W.master or m == 0) else O.AUX_NONE
             O.perturb(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=pmode)
             O.restore(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=mode)
         O.normalize(W.rewards(0 if W.copes_step else t), W.norm_mode)
@@ -270,7 +273,7 @@ def kernels_once(cp, torch):
     for _ in range(2):
         cp.cpes_perturb(w, s, sigma, 3, 1, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
         cp.cpes_restore(w, s, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
-        cp.cpes_perturb(w, s, sigma, 4, -1, aux=snap, aux_mode=cp.AUX_BACKUP)
+        cp.cpes_perturb(w, s, sigma, 4, -1)
         cp.cpes_restore(w, s, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
         cp.cpes_normalize_rewards(r, rn, cp.NORM_Z)
         cp.cpes_update(w, s, W.member_seeds(0), W.signs, rn, W.alpha, sigma)

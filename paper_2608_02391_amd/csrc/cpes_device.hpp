@@ -10,6 +10,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "cpes_log_table.hpp"
+
 namespace cpes {
 
 // ----------------------------------------------------------------- Philox --
@@ -66,35 +68,44 @@ __device__ __forceinline__ Words4 stream_block(uint32_t k0, uint32_t k1, uint32_
 // correctly rounded normal except within ~2^-17 relative of a rounding
 // boundary (and always within one fp32 ulp of it).
 //
-// Polynomial coefficients are near-minimax fits (relative error) computed
+// The angle polynomials are near-minimax fits (relative error) computed
 // offline with 120-bit arithmetic; the error of each evaluation is stated.
 
-// L = -2 ln U for U = m 2^-24, m in [1, 2^24].  m = f 2^e with f in
-// [1/sqrt2, sqrt2), ln U = (e - 24) ln 2 + 2 atanh(s), s = (f - 1) / (f + 1),
-// |s| <= 3 - 2 sqrt2; 2 atanh(s) / s is a degree-5 polynomial in s^2
-// (relative error 2^-45).  The reciprocal is the hardware estimate (2^-24)
-// refined by one Newton step.
-__device__ __forceinline__ double bm_log_term(uint32_t a)
+// L = -2 ln U for U = m 2^-24, m in [1, 2^24], table-driven (Tang's method):
+// mn = m << lz is m normalised to [2^31, 2^32); entry i = bits 30..23 of mn
+// holds inv_i ~ 2^-31 / c_i and B_i = -2 ln c_i for a point c_i of that
+// 1/256-wide mantissa interval (cpes_log_table.hpp).  Then
+//   r = mn inv_i - 1  (one fma, |r| <= 2^-8),
+//   L = (lz - 7) 2 ln 2 + B_i - 2 ln(1 + r),
+// with -2 ln(1 + r) = r q(r), q of degree 4 (Taylor).  Relative error at
+// most 2^-46.5 over all 2^24 inputs; U = 1 gives L = 0 exactly.  The table
+// lives in LDS (`lt`), staged once per workgroup by stage_log_table().
+__device__ __forceinline__ double bm_log_term(uint32_t a, const LogEntry* lt)
 {
-    const uint32_t m = (a >> 8) + 1u;
-    int ex;
-    const double mant = __builtin_frexp((double)m, &ex);    // (double)m = mant 2^ex, mant in [1/2, 1)
-    const int low = mant < 0x1.6a09e667f3bcdp-1 ? 1 : 0;    // below 1/sqrt2: use 2 mant
-    const double f = __builtin_ldexp(mant, low);
-    const double e = (double)(ex - low - 24);
-    const double num = f - 1.0;                              // exact
-    const double den = f + 1.0;                              // exact
-    double r = __builtin_amdgcn_rcp(den);
-    r = __builtin_fma(r, __builtin_fma(-den, r, 1.0), r);
-    const double s = num * r;
-    const double s2 = s * s;
-    double p = -0x1.9198127996755p-2;
-    p = __builtin_fma(p, s2, -0x1.c6208ce741fa9p-2);
-    p = __builtin_fma(p, s2, -0x1.24943960322ecp-1);
-    p = __builtin_fma(p, s2, -0x1.99999628a623ep-1);
-    p = __builtin_fma(p, s2, -0x1.5555555672df1p+0);
-    p = __builtin_fma(p, s2, -0x1.fffffffffff10p+1);        // -4 atanh(s) / s
-    return __builtin_fma(e, -0x1.62e42fefa39efp+0, s * p);   // e (-2 ln 2) - 4 atanh(s)
+    const uint32_t m7 = ((a >> 8) + 1u) << 7;             // m 2^7 <= 2^31
+    const uint32_t e = (uint32_t)__builtin_clz(m7);        // lz - 7, in [0, 24]
+    const uint32_t mn = m7 << e;
+    static_assert(sizeof(LogEntry) == 16, "16-byte table entries");
+    const uint32_t byte_off = (mn >> (27 - kLogTableBits)) & ((kLogTableSize - 1) << 4);   // entry * 16
+    const LogEntry t = *reinterpret_cast<const LogEntry*>(reinterpret_cast<const char*>(lt) + byte_off);
+    const double r = __builtin_fma((double)mn, t.inv, -1.0);
+    const double base = __builtin_fma((double)e, kTwoLn2, t.b);
+    double q = -0x1.999999999999ap-2;                      // -2/5
+    q = __builtin_fma(q, r, 0.5);
+    q = __builtin_fma(q, r, -0x1.5555555555555p-1);        // -2/3
+    q = __builtin_fma(q, r, 1.0);
+    q = __builtin_fma(q, r, -2.0);
+    return __builtin_fma(r, q, base);
+}
+
+// Copy the log table into LDS; every thread of the workgroup must call it
+// (it ends with a barrier).
+__device__ __forceinline__ const LogEntry* stage_log_table()
+{
+    __shared__ LogEntry lt[kLogTableSize];
+    for (int i = threadIdx.x; i < kLogTableSize; i += blockDim.x) lt[i] = kLogTable[i];
+    __syncthreads();
+    return lt;
 }
 
 // rho = sqrt(L): hardware reciprocal square root (2^-24) and one Goldschmidt
@@ -108,9 +119,9 @@ __device__ __forceinline__ double bm_sqrt(double L)
     return __builtin_fma(g, __builtin_fma(-g, h, 0.5), g);
 }
 
-__device__ __forceinline__ double bm_radius(uint32_t a)
+__device__ __forceinline__ double bm_radius(uint32_t a, const LogEntry* lt)
 {
-    return bm_sqrt(bm_log_term(a));
+    return bm_sqrt(bm_log_term(a, lt));
 }
 
 // Angle theta = pi m 2^-23, m = (b >> 8) + 1 in [1, 2^24].  Quadrant and
@@ -123,8 +134,8 @@ __device__ __forceinline__ double bm_radius(uint32_t a)
 struct AngleParts {
     double sp, cp;
     bool take_sin;       // cos theta = +-sp (and sin theta = +-cp)
-    uint32_t neg_cos;    // sign bit (bit 31) of cos theta
-    uint32_t neg_sin;    // sign bit (bit 31) of sin theta
+    uint32_t cos_sign;   // bit 31: sign of cos theta (other bits are not used)
+    uint32_t sin_sign;   // bit 31: sign of sin theta (other bits are not used)
 };
 
 __device__ __forceinline__ AngleParts bm_angle_parts(uint32_t b)
@@ -151,8 +162,8 @@ __device__ __forceinline__ AngleParts bm_angle_parts(uint32_t b)
     r.sp = sp;
     r.cp = cp;
     r.take_sin = fold ^ (((m >> 22) & 1u) != 0u);           // odd quadrant swaps the roles
-    r.neg_cos = ((m + (1u << 22)) << 8) & 0x80000000u;      // quadrant 1 or 2
-    r.neg_sin = (m << 8) & 0x80000000u;                     // quadrant 2 or 3
+    r.cos_sign = (m + (1u << 22)) << 8;                     // bit 31: quadrant 1 or 2
+    r.sin_sign = m << 8;                                    // bit 31: quadrant 2 or 3
     return r;
 }
 
@@ -162,43 +173,50 @@ __device__ __forceinline__ void bm_angle(uint32_t b, double& c_out, double& s_ou
     const AngleParts p = bm_angle_parts(b);
     const double mc = p.take_sin ? p.sp : p.cp;
     const double ms = p.take_sin ? p.cp : p.sp;
-    c_out = p.neg_cos ? -mc : mc;
-    s_out = p.neg_sin ? -ms : ms;
+    c_out = (p.cos_sign & 0x80000000u) ? -mc : mc;
+    s_out = (p.sin_sign & 0x80000000u) ? -ms : ms;
+}
+
+// z with its sign flipped where bit 31 of `sign` is set: one v_bitop3_b32
+// computing z ^ (sign & 0x80000000) (truth table 0x78 for src0 ^ (src1 & src2)).
+__device__ __forceinline__ float xor_sign(float z, uint32_t sign)
+{
+    return __uint_as_float(__builtin_amdgcn_bitop3_b32(__float_as_uint(z), sign, 0x80000000u, 0x78));
 }
 
 // Two normals of the pair (a, b): z_even = fp32(rho cos theta), z_odd =
 // fp32(rho sin theta).  The products are formed from the magnitudes and the
 // quadrant's swap and signs are applied to the fp32 results, which is exact
 // (negation commutes with multiplication and rounding).
-__device__ __forceinline__ void bm_pair(uint32_t a, uint32_t b, float& z_even, float& z_odd)
+__device__ __forceinline__ void bm_pair(uint32_t a, uint32_t b, const LogEntry* lt, float& z_even, float& z_odd)
 {
-    const double rho = bm_radius(a);
+    const double rho = bm_radius(a, lt);
     const AngleParts p = bm_angle_parts(b);
     const float zc = (float)(rho * p.cp);
     const float zs = (float)(rho * p.sp);
     const float me = p.take_sin ? zs : zc;
     const float mo = p.take_sin ? zc : zs;
-    z_even = __uint_as_float(__float_as_uint(me) ^ p.neg_cos);
-    z_odd = __uint_as_float(__float_as_uint(mo) ^ p.neg_sin);
+    z_even = xor_sign(me, p.cos_sign);
+    z_odd = xor_sign(mo, p.sin_sign);
 }
 
 // Four normals of block q: positions 4q .. 4q+3.
-__device__ __forceinline__ void normals4(uint32_t k0, uint32_t k1, uint64_t q, float z[4])
+__device__ __forceinline__ void normals4(uint32_t k0, uint32_t k1, uint64_t q, const LogEntry* lt, float z[4])
 {
     const Words4 x = stream_block(k0, k1, 0u, q);
-    bm_pair(x.x, x.y, z[0], z[1]);
-    bm_pair(x.z, x.w, z[2], z[3]);
+    bm_pair(x.x, x.y, lt, z[0], z[1]);
+    bm_pair(x.z, x.w, lt, z[2], z[3]);
 }
 
 // Eight normals of blocks q and q+1: positions 4q .. 4q+7.
-__device__ __forceinline__ void normals8(uint32_t k0, uint32_t k1, uint64_t q, float z[8])
+__device__ __forceinline__ void normals8(uint32_t k0, uint32_t k1, uint64_t q, const LogEntry* lt, float z[8])
 {
     const Words4 x = stream_block(k0, k1, 0u, q);
     const Words4 y = stream_block(k0, k1, 0u, q + 1u);
-    bm_pair(x.x, x.y, z[0], z[1]);
-    bm_pair(x.z, x.w, z[2], z[3]);
-    bm_pair(y.x, y.y, z[4], z[5]);
-    bm_pair(y.z, y.w, z[6], z[7]);
+    bm_pair(x.x, x.y, lt, z[0], z[1]);
+    bm_pair(x.z, x.w, lt, z[2], z[3]);
+    bm_pair(y.x, y.y, lt, z[4], z[5]);
+    bm_pair(y.z, y.w, lt, z[6], z[7]);
 }
 
 // ------------------------------------------------------------------ bf16 --

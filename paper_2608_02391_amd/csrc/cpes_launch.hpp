@@ -9,6 +9,9 @@ namespace cpes {
 
 constexpr int kBlock = 256;             // threads per workgroup for streaming kernels
 constexpr int64_t kMaxGrid = 1 << 20;   // workgroups per launch; larger jobs loop
+// Workgroups per launch of the noise kernels, which stage a 4 KiB table in
+// LDS per workgroup: a few per CU, each looping over many units.
+constexpr int64_t kRngMaxGrid = 8192;
 
 // Subspace addressing modes (see cpes_subspace).
 enum AddrMode { kAddrContig = 0, kAddrGather = 1, kAddrChunk = 2 };
