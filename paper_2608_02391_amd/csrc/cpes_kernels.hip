@@ -132,6 +132,21 @@ __device__ __forceinline__ bool param_of(const StreamArgs& a, int64_t j, int64_t
 // First parameter of the unit starting at position j0 for contiguous and
 // chunked subspaces (a unit never crosses a chunk); false if the unit would
 // leave [0, numel), in which case the caller takes the element path.
+//
+// The 64 lanes of a wave always hold 64 consecutive units whose first
+// position is a multiple of 64 n.  When a chunk holds at least 64 n positions
+// the whole wave therefore lies in one chunk, and its chunk id is read once,
+// by a scalar load from the wave's first active lane: the chunk list is
+// read-only here, so it is addressed as constant memory.
+typedef const int64_t __attribute__((address_space(4)))* ConstI64;
+
+__device__ __forceinline__ int64_t wave_uniform(int64_t x)
+{
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 template <int ADDR>
 __device__ __forceinline__ bool unit_base(const int64_t* index, int64_t offset, int64_t numel, int shift, int64_t j0,
                                           int n, int64_t& base)
@@ -140,7 +155,11 @@ __device__ __forceinline__ bool unit_base(const int64_t* index, int64_t offset, 
         base = offset + j0;
         return true;
     }
-    const int64_t c = index[offset + (j0 >> shift)];
+    int64_t c;
+    if ((int64_t)64 * n <= (1ll << shift))
+        c = ((ConstI64)(uintptr_t)index)[offset + (wave_uniform(j0) >> shift)];
+    else
+        c = index[offset + (j0 >> shift)];
     if (c < 0 || c > (numel >> shift)) return false;
     base = (c << shift) + (j0 & ((1ll << shift) - 1));
     return base + n <= numel;
