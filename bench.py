@@ -137,6 +137,8 @@ def run_step(W, cp, torch, P, timer, cache):
     sigmas = [float(__import__("numpy").float32(W.sigma * (W.d / n) ** 0.5)) for _, n in parts]
     aux_mode = cp.AUX_MASTER if W.master else cp.AUX_SNAPSHOT
 
+    later = cp.AUX_BACKUP if W.partition_mode == S.PART_PERMUTATION else cp.AUX_NONE
+
     def members(k, seeds, signs):
         s, aux = subs[k], P["aux"][:parts[k][1]]
         if W.host_backup:
@@ -152,8 +154,9 @@ def run_step(W, cp, torch, P, timer, cache):
             timer.run("stage_master", lambda: cp.cpes_stage_master(P["w"], s, aux))
         for m, (seed, sign) in enumerate(zip(seeds, signs)):
             # the first member takes the backup of the subspace; the others perturb the
-            # restored weights in place (a master source is read by every member)
-            mode = aux_mode if (W.master or m == 0) else cp.AUX_NONE
+            # restored weights in place, or, on an index map, read the (contiguous)
+            # backup instead of gathering w (a master source is read by every member)
+            mode = aux_mode if (W.master or m == 0) else later
             timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigmas[k], seed, sign, aux=aux, aux_mode=mode))
             # (the perturbed model would be evaluated here)
             timer.run("restore", lambda: cp.cpes_restore(P["w"], s, aux=aux, aux_mode=aux_mode))
@@ -194,7 +197,8 @@ def bytes_per_position(W, op):
         return e + ix                                  # HBM side; the same e bytes cross the host link
     if op == "perturb":
         # master: read master, write w; else the first member reads w and writes w and the
-        # backup, the others read and write w
+        # backup, the others read and write w (or, on an index map, read the backup and
+        # write w: the same bytes, one map read)
         return (4 + e if W.master else (3 * e + (m - 1) * 2 * e) / m) + ix
     if op == "restore":
         return (4 + e if W.master else 2 * e) + ix
@@ -234,7 +238,8 @@ def cpu_baseline(W, positions):
         if W.master:
             aux[:] = O.stage_master(w, 0, n)
         for m, (seed, sign) in enumerate(zip(seeds, signs)):
-            pmode = mode if (W.master or m == 0) else O.AUX_NONE
+            pmode = mode if (W.master or m == 0) else (O.AUX_BACKUP if W.partition_mode == S.PART_PERMUTATION
+                                                       else O.AUX_NONE)
             O.perturb(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=pmode)
             O.restore(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=mode)
         O.normalize(W.rewards(0 if W.copes_step else t), W.norm_mode)

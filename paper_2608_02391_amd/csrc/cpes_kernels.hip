@@ -924,6 +924,16 @@ int64_t grid_for(int64_t work_items, int64_t cap = kMaxGrid)
     return blocks < cap ? blocks : cap;
 }
 
+// Noise kernels on contiguous or chunked subspaces loop over the subspace from
+// a few workgroups per CU (the log table is staged once per workgroup).  On
+// index maps one workgroup per 256 units is faster: workgroups then start in
+// position order, so the scattered accesses in flight stay in a narrow window
+// of the weights (DRAM row and cache locality).
+inline int64_t rng_grid_cap(int addr)
+{
+    return addr == kGather ? kMaxGrid : kRngMaxGrid;
+}
+
 template <typename K, typename A>
 hipError_t launch1d(K kernel, int64_t items, const A& args, hipStream_t s, int64_t cap)
 {
@@ -951,14 +961,15 @@ int64_t units_of(int64_t length)
 template <typename T, int AUX>
 hipError_t perturb_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
-    const int64_t u = units_of<T>(a.length), cap = kRngMaxGrid;
+    const int64_t u = units_of<T>(a.length), cap = rng_grid_cap(addr);
     CPES_DISPATCH_ADDR_VEC(k_perturb, T, AUX)
 }
 
 template <typename T, bool MASTER>
 hipError_t update_t(int addr, bool vec, const UpdateArgs& a, hipStream_t s)
 {
-    const int64_t u = (a.length + (MASTER ? 8 : UnitOf<T>::n) - 1) / (MASTER ? 8 : UnitOf<T>::n), cap = kRngMaxGrid;
+    const int64_t u = (a.length + (MASTER ? 8 : UnitOf<T>::n) - 1) / (MASTER ? 8 : UnitOf<T>::n),
+                  cap = rng_grid_cap(addr);
     CPES_DISPATCH_ADDR_VEC(k_update, T, MASTER)
 }
 
@@ -1013,7 +1024,7 @@ hipError_t restore_master_t(int addr, bool vec, const StreamArgs& a, hipStream_t
 template <typename T>
 hipError_t update_step_t(int addr, const StepArgs& a, hipStream_t s)
 {
-    const int64_t blocks = grid_for(a.tile_begin[a.K] * 64, kRngMaxGrid);
+    const int64_t blocks = grid_for(a.tile_begin[a.K] * 64, rng_grid_cap(addr));
     switch (addr) {
     case kGather: hipLaunchKernelGGL((k_update_step<T, kGather>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
     case kChunk: hipLaunchKernelGGL((k_update_step<T, kChunk>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
