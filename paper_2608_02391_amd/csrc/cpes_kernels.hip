@@ -539,16 +539,24 @@ __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
     const int64_t wave = (int64_t)blockIdx.x * (kBlock / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
     const int64_t tiles = a.tile_begin[a.K];
     for (int64_t t = wave; t < tiles; t += waves) {
+        // t is the same for the whole wave; so are k and the stream range, which
+        // keeps the seed and coefficient reads scalar
         int k = 0;
         while (k + 1 < a.K && a.tile_begin[k + 1] <= t) ++k;
+        k = __builtin_amdgcn_readfirstlane(k);
+        const int st0 = __builtin_amdgcn_readfirstlane(a.stream_begin[k]);
+        const int st1 = __builtin_amdgcn_readfirstlane(a.stream_begin[k + 1]);
         const int64_t off = a.offset[k];
         const int64_t len = a.length[k];
         const int64_t j0 = ((t - a.tile_begin[k]) * 64 + lane) * N;
         if (j0 >= len) continue;
+        int64_t base = 0;
+        const bool vec = ((a.vec_mask >> k) & 1u) && j0 + N <= len &&
+                         (ADDR == kGather || unit_base<ADDR>(a.index, off, a.numel, a.chunk_shift, j0, N, base));
         float acc[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) acc[e] = 0.0f;
-        for (int st = a.stream_begin[k]; st < a.stream_begin[k + 1]; ++st) {
+        for (int st = st0; st < st1; ++st) {
             const float c = coef[st];
             float z[N];
             unit_normals<N>(a.seed_lo[st], a.seed_hi[st], (uint64_t)j0 >> 2, lt, z);
@@ -556,9 +564,6 @@ __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
             for (int e = 0; e < N; ++e) acc[e] = __builtin_fmaf(c, z[e], acc[e]);
         }
         const float step = a.step[k];
-        int64_t base = 0;
-        const bool vec = ((a.vec_mask >> k) & 1u) && j0 + N <= len &&
-                         (ADDR == kGather || unit_base<ADDR>(a.index, off, a.numel, a.chunk_shift, j0, N, base));
         if (vec) {
             T v[N], out[N];
             int64_t idx[N];
