@@ -49,7 +49,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=3)
     p.add_argument("--warmup", type=int, default=1)
-    p.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c4c", "p0", "c3h", "p0h"])
+    p.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c4c", "p0", "c3h", "p0h", "c4u"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--kernels-once", action="store_true",
                    help="run each kernel once on one 504,654,080-position subspace (for counter passes) and exit")
@@ -67,22 +67,30 @@ class KernelTimer:
         self.pending = {}
         self.done = {}
 
-    def run(self, name, fn):
+    def run(self, name, fn, positions=0):
         ev0 = self.torch.cuda.Event(enable_timing=True)
         ev1 = self.torch.cuda.Event(enable_timing=True)
         ev0.record()
         fn()
         ev1.record()
-        self.pending.setdefault(name, []).append((ev0, ev1))
+        self.pending.setdefault(name, []).append((ev0, ev1, positions))
 
     def collect(self):
         for name, evs in self.pending.items():
-            self.done.setdefault(name, []).extend(a.elapsed_time(b) for a, b in evs)
+            self.done.setdefault(name, []).extend((a.elapsed_time(b), n) for a, b, n in evs)
         self.pending = {}
 
     def stats(self, name):
-        ts = self.done.get(name, [])
+        ts = [t for t, _ in self.done.get(name, [])]
         return (sum(ts) / len(ts) if ts else 0.0), len(ts), sum(ts)
+
+    def rates(self, name):
+        """Per-launch positions per second: min, median and 90th percentile."""
+        r = sorted(n / (t * 1e-3) for t, n in self.done.get(name, []) if n and t > 0)
+        if not r:
+            return None
+        pick = lambda q: r[min(len(r) - 1, int(q * (len(r) - 1) + 0.5))]
+        return {"min": r[0], "p50": pick(0.5), "p90": pick(0.9)}
 
 
 def build_plan(W, cp, torch):
@@ -95,7 +103,7 @@ def build_plan(W, cp, torch):
     w = S.device_weights(W.d, W.dtype, W.weight_seed)
     index = ws = None
     if W.partition_mode == S.PART_PERMUTATION:
-        index = torch.empty(W.d, dtype=torch.int64, device=dev)
+        index = torch.empty(W.d, dtype=torch.int32 if W.map32 else torch.int64, device=dev)
         ws = torch.empty(cp.cpes_partition_workspace_bytes(cp.PART_PERMUTATION, W.d, W.K), dtype=torch.uint8,
                          device=dev)
     elif W.partition_mode == S.PART_CHUNKED:
@@ -117,7 +125,11 @@ def random_partition(W, cp, P):
     import synthetic as S
 
     if W.partition_mode == S.PART_PERMUTATION:
-        offs = cp.cpes_partition(cp.PART_PERMUTATION, W.d, W.K, W.partition_seed, index=P["index"], workspace=P["ws"])
+        if W.map32:
+            offs = cp.cpes_partition32(W.d, W.K, W.partition_seed, P["index"], P["ws"])
+        else:
+            offs = cp.cpes_partition(cp.PART_PERMUTATION, W.d, W.K, W.partition_seed, index=P["index"],
+                                     workspace=P["ws"])
         return [(offs[k], offs[k + 1] - offs[k]) for k in range(W.K)]
     offs, lens = cp.cpes_partition_chunks(W.d, W.chunk, W.K, W.partition_seed, P["index"], P["ws"])
     P["chunk_offsets"], P["chunk_lengths"] = offs, lens
@@ -141,25 +153,27 @@ def run_step(W, cp, torch, P, timer, cache):
 
     def members(k, seeds, signs):
         s, aux = subs[k], P["aux"][:parts[k][1]]
+        n_k = parts[k][1]
         if W.host_backup:
             # Sec. 3.3: the pre-perturbation weights go to host memory once, every
             # member is perturbed in place and restored from there
             host = P["host"][:parts[k][1]]
-            timer.run("backup_host", lambda: cp.cpes_backup_to_host(P["w"], s, host))
+            timer.run("backup_host", lambda: cp.cpes_backup_to_host(P["w"], s, host), n_k)
             for seed, sign in zip(seeds, signs):
-                timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigmas[k], seed, sign))
-                timer.run("restore_host", lambda: cp.cpes_restore_from_host(P["w"], s, host))
+                timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigmas[k], seed, sign), n_k)
+                timer.run("restore_host", lambda: cp.cpes_restore_from_host(P["w"], s, host), n_k)
             return
         if W.master:
-            timer.run("stage_master", lambda: cp.cpes_stage_master(P["w"], s, aux))
+            timer.run("stage_master", lambda: cp.cpes_stage_master(P["w"], s, aux), n_k)
         for m, (seed, sign) in enumerate(zip(seeds, signs)):
             # the first member takes the backup of the subspace; the others perturb the
             # restored weights in place, or, on an index map, read the (contiguous)
             # backup instead of gathering w (a master source is read by every member)
             mode = aux_mode if (W.master or m == 0) else later
-            timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigmas[k], seed, sign, aux=aux, aux_mode=mode))
+            timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigmas[k], seed, sign, aux=aux, aux_mode=mode),
+                      n_k)
             # (the perturbed model would be evaluated here)
-            timer.run("restore", lambda: cp.cpes_restore(P["w"], s, aux=aux, aux_mode=aux_mode))
+            timer.run("restore", lambda: cp.cpes_restore(P["w"], s, aux=aux, aux_mode=aux_mode), n_k)
 
     if W.copes_step:
         # Alg. 1: every subspace gets N/K members, joint standardisation, one composed update
@@ -173,7 +187,8 @@ def run_step(W, cp, torch, P, timer, cache):
             offsets = P["chunk_offsets"]
         timer.run("update", lambda: cp.cpes_update_step(
             P["w"], offsets, seeds, W.signs, ks, P["rnorm"][0], W.alpha, sigmas, W.scale_mode,
-            index=P["index"], chunk=W.chunk, lengths=[n for _, n in parts] if W.chunk else None))
+            index=P["index"], chunk=W.chunk, lengths=[n for _, n in parts] if W.chunk else None),
+            sum(n for _, n in parts))
         return
     for t, k in enumerate(W.active):
         seeds = W.member_seeds(t)
@@ -181,7 +196,8 @@ def run_step(W, cp, torch, P, timer, cache):
         timer.run("normalize", lambda: cp.cpes_normalize_rewards(P["rewards"][t], P["rnorm"][t], W.norm_mode))
         timer.run("update", lambda: cp.cpes_update(P["w"], subs[k], seeds, W.signs, P["rnorm"][t], W.alpha,
                                                    sigmas[k], W.scale_mode,
-                                                   master=P["aux"][:parts[k][1]] if W.master else None))
+                                                   master=P["aux"][:parts[k][1]] if W.master else None),
+                  parts[k][1])
 
 
 def bytes_per_position(W, op):
@@ -189,7 +205,7 @@ def bytes_per_position(W, op):
     import synthetic as S
 
     e = 2 if W.dtype == S.BF16 else 4
-    ix = 8 if W.partition_mode == S.PART_PERMUTATION else 0
+    ix = (4 if W.map32 else 8) if W.partition_mode == S.PART_PERMUTATION else 0
     m = W.n // W.K if W.copes_step else W.n          # members perturbing one subspace
     if op == "perturb" and W.host_backup:
         return 2 * e + ix
@@ -207,6 +223,29 @@ def bytes_per_position(W, op):
     if op == "stage_master":
         return e + 4 + ix
     return 0
+
+
+def copy_reference(W, torch, P, sizes):
+    """The achievable-HBM reference, in the same run: torch's device-to-device
+    copy (hipMemcpy) of the largest subspace's weights, median of 5."""
+    import statistics
+
+    L = max(sizes[k] for k in W.active)
+    src = P["w"][:L]
+    dst = P["aux"].view(src.dtype)[:L]
+    dst.copy_(src)
+    ts = []
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    nbytes = 2 * L * src.element_size()
+    ms = statistics.median(ts)
+    return {"GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes, "ms": round(ms, 4),
+            "kind": "torch copy_ (hipMemcpy D2D) of the largest subspace's weights"}
 
 
 def cpu_baseline(W, positions):
@@ -359,6 +398,9 @@ def main():
                 streams = len(set(W.member_seeds(0))) // (W.K if W.copes_step else 1)
             entry["params/s"] = round(per_launch / (avg_ms * 1e-3), 1)
             entry["Gnormal/s"] = round(streams * per_launch / (avg_ms * 1e-3) / 1e9, 2)
+        rr = timer.rates(op)
+        if rr:                                       # spread over launches, in G positions/s
+            entry["per_launch_Gpos/s"] = {q: round(v / 1e9, 2) for q, v in rr.items()}
         ops[op] = entry
     # the dominant GPU kernel; host-link transfers are reported in ops
     dominant = max((o for o in ops if o not in ("normalize", "backup_host", "restore_host")),
@@ -404,6 +446,7 @@ def main():
     }
     if part_ms is not None:
         line["partition_ms"] = round(part_ms, 3)
+    line["copy_reference"] = copy_reference(W, torch, P, sizes)
     if not args.no_cpu_baseline:
         positions = args.cpu_positions or (1 << 31) // W.n
         line["cpu_baseline"] = cpu_baseline(W, positions)

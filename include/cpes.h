@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define CPES_ABI_VERSION 2
+#define CPES_ABI_VERSION 3
 
 /* Exported symbols (the library is built with hidden default visibility). */
 #define CPES_API __attribute__((visibility("default")))
@@ -85,10 +85,13 @@ enum cpes_scale_mode { CPES_SCALE_ALPHA_OVER_N_SIGMA = 0, CPES_SCALE_ALPHA_OVER_
 #define CPES_MAX_STEP_SUBSPACES 32   /* subspaces per cpes_update_step call */
 
 typedef struct cpes_subspace {
-    int64_t offset;        /* first parameter (index == NULL) or first map entry */
-    int64_t length;        /* number of positions d_k, >= 0 */
-    const int64_t* index;  /* NULL, or device int64 map (parameters or chunk ids) */
-    int64_t chunk;         /* 0, or a power of two >= 8: index entries name chunks of this size */
+    int64_t offset;          /* first parameter (no map) or first map entry */
+    int64_t length;          /* number of positions d_k, >= 0 */
+    const int64_t* index;    /* NULL, or device int64 map (parameters or chunk ids) */
+    int64_t chunk;           /* 0, or a power of two >= 8: index entries name chunks of this size */
+    const uint32_t* index32; /* NULL, or device uint32 map of parameters (half the map traffic
+                                of `index`; models of at most 2^32 parameters); at most one of
+                                index / index32, and chunk = 0 with index32 */
 } cpes_subspace;
 
 /*
@@ -120,6 +123,18 @@ typedef struct cpes_subspace {
 CPES_API int cpes_partition(int mode, int64_t d, int32_t K, uint64_t seed, const int64_t* bounds_host,
                    int64_t* offsets_host, int64_t* index_dev, void* workspace_dev,
                    size_t workspace_bytes, int32_t* status_dev, void* stream);
+
+/*
+ * cpes_partition32 -- the CPES_PART_PERMUTATION partition of cpes_partition
+ * written as a uint32 map (index_dev: device uint32[d]) for d <= 2^32: half
+ * the memory and half the map traffic of the int64 map, same entries.  Use it
+ * through cpes_subspace.index32.  Workspace as
+ * cpes_partition_workspace_bytes(CPES_PART_PERMUTATION, d, K).
+ * Errors: d < 1 or d > 2^32, K < 1 or K > d, null pointers ->
+ *   CPES_ERR_INVALID_ARGUMENT; otherwise as cpes_partition.
+ */
+CPES_API int cpes_partition32(int64_t d, int32_t K, uint64_t seed, int64_t* offsets_host, uint32_t* index_dev,
+                     void* workspace_dev, size_t workspace_bytes, int32_t* status_dev, void* stream);
 
 /* Workspace bytes cpes_partition needs (0 for CONTIGUOUS); 0 for invalid arguments. */
 CPES_API size_t cpes_partition_workspace_bytes(int mode, int64_t d, int32_t K);
@@ -277,7 +292,8 @@ CPES_API int cpes_update(void* w_dev, int64_t numel, int dtype, const cpes_subsp
  * offsets_host (K+1, non-decreasing): subspace k is positions [offsets[k],
  *   offsets[k+1]) -- parameters themselves (index_dev == NULL; offsets[K] <=
  *   numel) or entries of the int64 device map index_dev (e.g. the output of
- *   cpes_partition).  Noise position j is counted from offsets[k].
+ *   cpes_partition; uint32 maps are not taken here).  Noise position j is
+ *   counted from offsets[k].
  *   With chunk > 0, index_dev holds chunk ids (cpes_partition_chunks),
  *   subspace k is cpes_subspace{offsets[k], lengths_host[k], index_dev, chunk}
  *   and lengths_host (host, K) is required; otherwise lengths_host is ignored.
@@ -328,6 +344,21 @@ CPES_API int cpes_rng_probe(uint64_t seed, int64_t n, uint32_t* sink_dev, void* 
 
 /* Message of the last error on the calling thread ("" if none). */
 CPES_API const char* cpes_last_error(void);
+
+/*
+ * cpes_fill_normal -- w[j] = cast(stddev * z_j) for j < n, where z_j is the
+ * normal of position j in stream (seed, domain): the Philox4x32-10 words of
+ * counter (lo32 q, hi32 q, domain, 0), q = j / 4, through the Box-Muller
+ * transform of the perturbation noise (domain 0 is the noise itself; domain
+ * 1 is meant for synthetic weight initialisation).  One fp32 multiply, then
+ * round-to-nearest-even for bf16.  A utility for seeded inputs; not on the
+ * training path.
+ *   w_dev: n elements of `dtype` (any alignment), owned by the caller.
+ * Errors: dtype unknown, n < 0, stddev negative or not finite, w NULL with
+ *   n > 0 -> CPES_ERR_INVALID_ARGUMENT.  n = 0 does nothing.
+ */
+CPES_API int cpes_fill_normal(void* w_dev, int64_t n, int dtype, uint64_t seed, uint32_t domain, float stddev,
+                     void* stream);
 
 /* CPES_ABI_VERSION of the built library. */
 CPES_API int cpes_abi_version(void);

@@ -68,6 +68,9 @@ def lib() -> ctypes.CDLL:
         L.orc_normal.argtypes = [u64, i64]
         L.orc_normal.restype = ctypes.c_float
         L.orc_normals.argtypes = [u64, i64, i64, _c_f32p]
+        L.orc_normal_domain.argtypes = [u64, ctypes.c_uint32, i64]
+        L.orc_normal_domain.restype = ctypes.c_float
+        L.orc_fill_normal.argtypes = [vp, ctypes.c_int, i64, u64, ctypes.c_uint32, ctypes.c_float]
         L.orc_f32_to_bf16.argtypes = [f32]
         L.orc_f32_to_bf16.restype = ctypes.c_uint16
         L.orc_perturb.argtypes = [vp, i32, i64, i64, vp, i64, f32, u64, i32, vp, i32]
@@ -164,6 +167,17 @@ def normals(seed: int, j0: int, n: int) -> np.ndarray:
     out = np.empty(n, dtype=np.float32)
     lib().orc_normals(seed, j0, n, out.ctypes.data_as(_c_f32p))
     return out
+
+
+def normal_domain(seed: int, domain: int, j: int) -> float:
+    return lib().orc_normal_domain(seed, domain, j)
+
+
+def fill_normal(n: int, dtype: int, seed: int, domain: int, stddev: float) -> np.ndarray:
+    """Seeded weights: cast(stddev * z_j) for j < n from stream (seed, domain)."""
+    w = np.empty(n, dtype=np.uint16 if dtype == BF16 else np.float32)
+    _check(lib().orc_fill_normal(_ptr(w), dtype, n, seed, domain, stddev), "fill_normal")
+    return w
 
 
 def f32_to_bf16(x: float) -> int:

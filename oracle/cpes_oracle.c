@@ -148,8 +148,15 @@ void orc_bm_angle_many(const uint32_t* b, int64_t n, double* cos_out, double* si
  * double product is rounded once to fp32. */
 float orc_normal(uint64_t seed, int64_t j)
 {
+    return orc_normal_domain(seed, ORC_DOMAIN_NOISE, j);
+}
+
+/* The same transform on the words of another stream domain (domain 1:
+ * synthetic weight initialisation). */
+float orc_normal_domain(uint64_t seed, uint32_t domain, int64_t j)
+{
     uint32_t x[4];
-    orc_block(seed, ORC_DOMAIN_NOISE, (uint64_t)j >> 2, x);
+    orc_block(seed, domain, (uint64_t)j >> 2, x);
     int t = (int)(j & 3);
     uint32_t a = (t < 2) ? x[0] : x[2];
     uint32_t b = (t < 2) ? x[1] : x[3];
@@ -173,6 +180,24 @@ void orc_normals(uint64_t seed, int64_t j0, int64_t n, float* out)
 #pragma omp parallel for schedule(static)
     for (k = 0; k < n; ++k)
         out[k] = orc_normal(seed, j0 + k);
+}
+
+/* Seeded normal fill: w[j] = cast(stddev * z_j) with z_j the normal of
+ * position j in stream (seed, domain); the product is one fp32 multiply,
+ * then bf16 rounding for bf16 storage. */
+int orc_fill_normal(void* w, int dtype, int64_t n, uint64_t seed, uint32_t domain, float stddev)
+{
+    int64_t j;
+    if (n < 0 || (dtype != ORC_BF16 && dtype != ORC_F32)) return -1;
+#pragma omp parallel for schedule(static)
+    for (j = 0; j < n; ++j) {
+        float v = stddev * orc_normal_domain(seed, domain, j);
+        if (dtype == ORC_BF16)
+            ((uint16_t*)w)[j] = orc_f32_to_bf16(v);
+        else
+            ((float*)w)[j] = v;
+    }
+    return 0;
 }
 
 /* ------------------------------------------------------------------------- */

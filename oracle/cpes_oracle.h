@@ -41,6 +41,8 @@ void orc_bm_radius_many(const uint32_t* a, int64_t n, double* out);
 void orc_bm_angle_many(const uint32_t* b, int64_t n, double* cos_out, double* sin_out);
 void orc_blocks(uint64_t seed, uint32_t domain, uint64_t q0, int64_t nblocks, uint32_t* out);
 float orc_normal(uint64_t seed, int64_t j);
+float orc_normal_domain(uint64_t seed, uint32_t domain, int64_t j);
+int orc_fill_normal(void* w, int dtype, int64_t n, uint64_t seed, uint32_t domain, float stddev);
 void orc_normals(uint64_t seed, int64_t j0, int64_t n, float* out);
 uint16_t orc_f32_to_bf16(float f);
 float orc_bf16_to_f32(uint16_t h);

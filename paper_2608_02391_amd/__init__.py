@@ -24,10 +24,10 @@ SCALE_ALPHA_OVER_N_SIGMA, SCALE_ALPHA_OVER_N = 0, 1
 MAX_MEMBERS, MAX_REWARDS, MAX_GROUPS, MAX_PERMUTATION_K, MAX_STEP_SUBSPACES = 256, 4096, 1024, 256, 32
 
 EXPORTED = (
-    "cpes_partition", "cpes_partition_workspace_bytes", "cpes_partition_chunks",
+    "cpes_partition", "cpes_partition32", "cpes_partition_workspace_bytes", "cpes_partition_chunks",
     "cpes_partition_chunks_workspace_bytes", "cpes_perturb", "cpes_restore",
     "cpes_backup_to_host", "cpes_restore_from_host", "cpes_stage_master", "cpes_normalize_rewards", "cpes_update", "cpes_update_step", "cpes_debug_philox",
-    "cpes_debug_normals", "cpes_debug_bm_grid", "cpes_debug_prp", "cpes_rng_probe",
+    "cpes_debug_normals", "cpes_debug_bm_grid", "cpes_debug_prp", "cpes_rng_probe", "cpes_fill_normal",
     "cpes_last_error", "cpes_abi_version",
 )
 
@@ -40,7 +40,7 @@ class CpesError(RuntimeError):
 
 class Subspace(ctypes.Structure):
     _fields_ = [("offset", ctypes.c_int64), ("length", ctypes.c_int64), ("index", ctypes.c_void_p),
-                ("chunk", ctypes.c_int64)]
+                ("chunk", ctypes.c_int64), ("index32", ctypes.c_void_p)]
 
 
 _lib = None
@@ -59,6 +59,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     sp = ctypes.POINTER(Subspace)
     sig = {
         "cpes_partition": [i32, i64, i32, u64, vp, vp, vp, vp, ctypes.c_size_t, vp, vp],
+        "cpes_partition32": [i64, i32, u64, vp, vp, vp, ctypes.c_size_t, vp, vp],
         "cpes_partition_workspace_bytes": [i32, i64, i32],
         "cpes_partition_chunks": [i64, i64, i32, u64, vp, vp, vp, vp, ctypes.c_size_t, vp, vp],
         "cpes_partition_chunks_workspace_bytes": [i64, i64, i32],
@@ -75,6 +76,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "cpes_debug_bm_grid": [u32, i64, vp, vp, vp, vp],
         "cpes_debug_prp": [u64, i64, i32, i64, i64, vp, vp, vp],
         "cpes_rng_probe": [u64, i64, vp, vp],
+        "cpes_fill_normal": [vp, i64, i32, u64, u32, f32, vp],
         "cpes_last_error": [],
         "cpes_abi_version": [],
     }
@@ -149,10 +151,19 @@ def _stream(stream) -> Optional[int]:
 
 def subspace(offset: int, length: int, index=None, chunk: int = 0) -> Subspace:
     """Positions j < length at parameter offset + j, index[offset + j], or
-    (chunk > 0) index[offset + j // chunk] * chunk + j % chunk."""
-    if index is not None and index.dtype != _torch().int64:
-        raise TypeError("index map must be int64")
-    sub = Subspace(int(offset), int(length), _dev_ptr(index, "index map"), int(chunk))
+    (chunk > 0) index[offset + j // chunk] * chunk + j % chunk.  An int64 map
+    goes to ``index``; a 32-bit map (torch.int32 or torch.uint32 holding the
+    uint32 entries of cpes_partition32) goes to ``index32``."""
+    torch = _torch()
+    idx64 = idx32 = None
+    if index is not None:
+        if index.dtype == torch.int64:
+            idx64 = _dev_ptr(index, "index map")
+        elif index.dtype in (torch.int32, getattr(torch, "uint32", torch.int32)):
+            idx32 = _dev_ptr(index, "index map")
+        else:
+            raise TypeError("index map must be int64, or 32-bit for a uint32 map")
+    sub = Subspace(int(offset), int(length), idx64, int(chunk), idx32)
     sub._index = index      # the descriptor holds a raw pointer: keep the map's storage alive with it
     return sub
 
@@ -169,6 +180,18 @@ def cpes_partition(mode: int, d: int, K: int, seed: int = 0, bounds: Optional[Se
     _check(L.cpes_partition(mode, d, K, seed, b, offsets, _dev_ptr(index, "index"),
                             _dev_ptr(workspace, "workspace"), ws_bytes, _dev_ptr(status, "status"),
                             _stream(stream)))
+    return [int(x) for x in offsets]
+
+
+def cpes_partition32(d: int, K: int, seed: int, index, workspace, status=None, stream=None):
+    """Permutation partition into a 32-bit map (d <= 2^32); returns the K+1 offsets."""
+    L = load()
+    offsets = (ctypes.c_int64 * (K + 1))()
+    if index.element_size() != 4:
+        raise TypeError("cpes_partition32 writes a 32-bit map")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(L.cpes_partition32(d, K, seed, offsets, _dev_ptr(index, "index"), _dev_ptr(workspace, "workspace"),
+                              ws_bytes, _dev_ptr(status, "status"), _stream(stream)))
     return [int(x) for x in offsets]
 
 
@@ -214,6 +237,12 @@ def cpes_restore_from_host(w, s: Subspace, backup, stream=None) -> None:
     """w[p(j)] = backup[j] from a pinned host tensor."""
     _check(load().cpes_restore_from_host(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s),
                                          _host_ptr(backup, w, s, "backup"), _stream(stream)))
+
+
+def cpes_fill_normal(w, seed: int, domain: int = 1, stddev: float = 0.02, stream=None) -> None:
+    """Fill the device tensor w with cast(stddev * z_j) from stream (seed, domain)."""
+    _check(load().cpes_fill_normal(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), seed, domain, stddev,
+                                   _stream(stream)))
 
 
 def cpes_stage_master(w, s: Subspace, master, stream=None) -> None:

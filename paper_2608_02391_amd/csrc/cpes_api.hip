@@ -55,7 +55,11 @@ int check_subspace(const void* w, int64_t numel, int dtype, const cpes_subspace*
                     (long long)s->length);
     if (s->length > (INT64_MAX / 8) - s->offset)
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: offset + length overflows", fn);
-    if (!s->index && s->offset + s->length > numel)
+    if (s->index && s->index32)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: a subspace takes an int64 or a uint32 map, not both", fn);
+    if (s->index32 && s->chunk != 0)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: chunk lists are int64 maps", fn);
+    if (!s->index && !s->index32 && s->offset + s->length > numel)
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: range [%lld, %lld) exceeds numel %lld", fn, (long long)s->offset,
                     (long long)(s->offset + s->length), (long long)numel);
     if (s->chunk != 0) {
@@ -69,6 +73,7 @@ int check_subspace(const void* w, int64_t numel, int dtype, const cpes_subspace*
 
 int addr_mode(const cpes_subspace* s)
 {
+    if (s->index32) return cpes::kAddrGather32;
     if (!s->index) return cpes::kAddrContig;
     return s->chunk ? cpes::kAddrChunk : cpes::kAddrGather;
 }
@@ -100,6 +105,8 @@ bool vector_ok(const void* w, int dtype, const cpes_subspace* s, const void* aux
         if (!aligned16(w)) return false;                    // chunk starts are multiples of 8 elements
     } else if (s->index) {
         if (!aligned16(s->index + s->offset)) return false;
+    } else if (s->index32) {
+        if (!aligned16(s->index32 + s->offset)) return false;
     } else {
         const char* base = static_cast<const char*>(w) + (size_t)s->offset * elem_size(dtype);
         if (!aligned16(base)) return false;
@@ -114,7 +121,7 @@ cpes::StreamArgs stream_args(void* w, int64_t numel, const cpes_subspace* s, con
 {
     cpes::StreamArgs a;
     a.w = w;
-    a.index = s->index;
+    a.index = s->index32 ? reinterpret_cast<const int64_t*>(s->index32) : s->index;
     a.aux = const_cast<void*>(aux);
     a.offset = s->offset;
     a.length = s->length;
@@ -190,6 +197,38 @@ PartitionLayout partition_layout(int64_t d, int32_t K)
     return L;
 }
 
+// The keyed-permutation partition into an int64 or a uint32 map.
+int permutation_partition(int64_t d, int32_t K, uint64_t seed, int64_t* offsets_host, int64_t* index64,
+                          uint32_t* index32, void* workspace_dev, size_t workspace_bytes, int32_t* status_dev,
+                          void* stream, const char* fn)
+{
+    if (K > CPES_MAX_PERMUTATION_K)
+        return fail(CPES_ERR_UNSUPPORTED, "%s: K %d above CPES_MAX_PERMUTATION_K", fn, K);
+    if (d >= ((int64_t)1 << 55)) return fail(CPES_ERR_UNSUPPORTED, "%s: permutation needs d < 2^55", fn);
+    const PartitionLayout L = partition_layout(d, K);
+    if (!workspace_dev || workspace_bytes < L.total)
+        return fail(CPES_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, L.total,
+                    workspace_dev ? workspace_bytes : (size_t)0);
+    if (!aligned16(workspace_dev)) return fail(CPES_ERR_WORKSPACE, "%s: workspace must be 16-byte aligned", fn);
+    for (int32_t k = 0; k <= K; ++k)
+        offsets_host[k] = (int64_t)(((unsigned __int128)(uint64_t)d * (uint64_t)k + (uint64_t)K - 1u) / (uint64_t)K);
+    char* ws = static_cast<char*>(workspace_dev);
+    cpes::PartitionArgs a;
+    a.seed = seed;
+    a.d = d;
+    a.K = K;
+    a.half_bits = feistel_half_bits(d);
+    a.bucket = reinterpret_cast<uint8_t*>(ws);
+    a.counts = reinterpret_cast<uint32_t*>(ws + L.off_counts);
+    a.pos = reinterpret_cast<int64_t*>(ws + L.off_pos);
+    a.block_sums = reinterpret_cast<int64_t*>(ws + L.off_block_sums);
+    a.n_tiles = L.n_tiles;
+    a.index = index64;
+    a.index32 = index32;
+    a.status = status_dev;
+    return hip_status(cpes::launch_partition(a, (hipStream_t)stream), fn);
+}
+
 // A host backup must be pinned memory the device can address (hipHostMalloc,
 // torch pin_memory); a kernel touching pageable memory would fault.  Returns
 // the device-side address of the buffer in *dev.
@@ -214,7 +253,7 @@ int host_backup_copy(void* w_dev, int64_t numel, int dtype, const cpes_subspace*
     void* host_dev = nullptr;
     if ((rc = check_pinned_host(host, &host_dev, fn))) return rc;
     hipStream_t st = (hipStream_t)stream;
-    if (!s->index) {   // contiguous: one DMA transfer over the host link
+    if (!s->index && !s->index32) {   // contiguous: one DMA transfer over the host link
         const size_t bytes = (size_t)s->length * elem_size(dtype);
         char* dev = static_cast<char*>(w_dev) + (size_t)s->offset * elem_size(dtype);
         const hipError_t e = to_host ? hipMemcpyAsync(host, dev, bytes, hipMemcpyDeviceToHost, st)
@@ -275,31 +314,23 @@ int cpes_partition(int mode, int64_t d, int32_t K, uint64_t seed, const int64_t*
         }
         return CPES_OK;
     }
-    if (K > CPES_MAX_PERMUTATION_K)
-        return fail(CPES_ERR_UNSUPPORTED, "%s: K %d above CPES_MAX_PERMUTATION_K", fn, K);
-    if (d >= ((int64_t)1 << 55)) return fail(CPES_ERR_UNSUPPORTED, "%s: permutation needs d < 2^55", fn);
     if (!index_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: index_dev is null", fn);
-    const PartitionLayout L = partition_layout(d, K);
-    if (!workspace_dev || workspace_bytes < L.total)
-        return fail(CPES_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, L.total,
-                    workspace_dev ? workspace_bytes : (size_t)0);
-    if (!aligned16(workspace_dev)) return fail(CPES_ERR_WORKSPACE, "%s: workspace must be 16-byte aligned", fn);
-    for (int32_t k = 0; k <= K; ++k)
-        offsets_host[k] = (int64_t)(((unsigned __int128)(uint64_t)d * (uint64_t)k + (uint64_t)K - 1u) / (uint64_t)K);
-    char* ws = static_cast<char*>(workspace_dev);
-    cpes::PartitionArgs a;
-    a.seed = seed;
-    a.d = d;
-    a.K = K;
-    a.half_bits = feistel_half_bits(d);
-    a.bucket = reinterpret_cast<uint8_t*>(ws);
-    a.counts = reinterpret_cast<uint32_t*>(ws + L.off_counts);
-    a.pos = reinterpret_cast<int64_t*>(ws + L.off_pos);
-    a.block_sums = reinterpret_cast<int64_t*>(ws + L.off_block_sums);
-    a.n_tiles = L.n_tiles;
-    a.index = index_dev;
-    a.status = status_dev;
-    return hip_status(cpes::launch_partition(a, (hipStream_t)stream), fn);
+    return permutation_partition(d, K, seed, offsets_host, index_dev, nullptr, workspace_dev, workspace_bytes,
+                                 status_dev, stream, fn);
+}
+
+int cpes_partition32(int64_t d, int32_t K, uint64_t seed, int64_t* offsets_host, uint32_t* index_dev,
+                     void* workspace_dev, size_t workspace_bytes, int32_t* status_dev, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_partition32";
+    if (d < 1 || d > ((int64_t)1 << 32))
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: d %lld not in [1, 2^32]", fn, (long long)d);
+    if (K < 1 || (int64_t)K > d) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: K %d not in [1, d]", fn, K);
+    if (!offsets_host) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: offsets_host is null", fn);
+    if (!index_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: index_dev is null", fn);
+    return permutation_partition(d, K, seed, offsets_host, nullptr, index_dev, workspace_dev, workspace_bytes,
+                                 status_dev, stream, fn);
 }
 
 size_t cpes_partition_chunks_workspace_bytes(int64_t d, int64_t chunk, int32_t K)
@@ -486,7 +517,7 @@ int cpes_update(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, f
     const double step = scale_mode == CPES_SCALE_ALPHA_OVER_N_SIGMA ? (double)alpha / ((double)n * (double)sigma)
                                                                     : (double)alpha / (double)n;
     a.w = w_dev;
-    a.index = s->index;
+    a.index = s->index32 ? reinterpret_cast<const int64_t*>(s->index32) : s->index;
     a.master = master_dev;
     a.rnorm = rnorm_dev;
     a.offset = s->offset;
@@ -597,6 +628,20 @@ int cpes_update_step(void* w_dev, int64_t numel, int dtype, int32_t K, const int
     if (tiles == 0) return CPES_OK;
     const int addr = !index_dev ? cpes::kAddrContig : chunk ? cpes::kAddrChunk : cpes::kAddrGather;
     return hip_status(cpes::launch_update_step(dtype, addr, a, (hipStream_t)stream), fn);
+}
+
+int cpes_fill_normal(void* w_dev, int64_t n, int dtype, uint64_t seed, uint32_t domain, float stddev, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_fill_normal";
+    if (dtype != CPES_BF16 && dtype != CPES_F32) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown dtype %d", fn, dtype);
+    if (n < 0) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: n %lld is negative", fn, (long long)n);
+    int rc = check_sigma(stddev, fn);
+    if (rc) return rc;
+    if (n == 0) return CPES_OK;
+    if (!w_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: w is null", fn);
+    return hip_status(cpes::launch_fill_normal(dtype, w_dev, n, seed, domain, stddev, aligned16(w_dev),
+                                               (hipStream_t)stream), fn);
 }
 
 int cpes_debug_philox(uint64_t seed, uint32_t domain, uint64_t q0, int64_t nblocks, uint32_t* out_dev, void* stream)

@@ -200,19 +200,21 @@ __device__ __forceinline__ void bm_pair(uint32_t a, uint32_t b, const LogEntry* 
     z_odd = xor_sign(mo, p.sin_sign);
 }
 
-// Four normals of block q: positions 4q .. 4q+3.
-__device__ __forceinline__ void normals4(uint32_t k0, uint32_t k1, uint64_t q, const LogEntry* lt, float z[4])
+// Four normals of block q: positions 4q .. 4q+3 (domain 0 is the noise).
+__device__ __forceinline__ void normals4(uint32_t k0, uint32_t k1, uint64_t q, const LogEntry* lt, float z[4],
+                                         uint32_t domain = 0u)
 {
-    const Words4 x = stream_block(k0, k1, 0u, q);
+    const Words4 x = stream_block(k0, k1, domain, q);
     bm_pair(x.x, x.y, lt, z[0], z[1]);
     bm_pair(x.z, x.w, lt, z[2], z[3]);
 }
 
 // Eight normals of blocks q and q+1: positions 4q .. 4q+7.
-__device__ __forceinline__ void normals8(uint32_t k0, uint32_t k1, uint64_t q, const LogEntry* lt, float z[8])
+__device__ __forceinline__ void normals8(uint32_t k0, uint32_t k1, uint64_t q, const LogEntry* lt, float z[8],
+                                         uint32_t domain = 0u)
 {
-    const Words4 x = stream_block(k0, k1, 0u, q);
-    const Words4 y = stream_block(k0, k1, 0u, q + 1u);
+    const Words4 x = stream_block(k0, k1, domain, q);
+    const Words4 y = stream_block(k0, k1, domain, q + 1u);
     bm_pair(x.x, x.y, lt, z[0], z[1]);
     bm_pair(x.z, x.w, lt, z[2], z[3]);
     bm_pair(y.x, y.y, lt, z[4], z[5]);

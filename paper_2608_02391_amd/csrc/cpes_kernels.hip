@@ -101,7 +101,49 @@ __device__ __forceinline__ int64_t global_tid() { return (int64_t)blockIdx.x * b
 // Subspace addressing: position j is parameter offset + j (kContig),
 // index[offset + j] (kGather), or, with chunks of 2^s parameters,
 // index[offset + (j >> s)] * 2^s + (j mod 2^s) (kChunk).
-constexpr int kContig = kAddrContig, kGather = kAddrGather, kChunk = kAddrChunk;
+constexpr int kContig = kAddrContig, kGather = kAddrGather, kChunk = kAddrChunk, kGather32 = kAddrGather32;
+
+// An element-level map (int64 or uint32 entries).
+template <int ADDR>
+constexpr bool kMap = ADDR == kGather || ADDR == kGather32;
+
+// The map entries of positions p .. p + N - 1 (16-byte loads; p + index must
+// be 16-byte aligned), widened to int64.
+template <int ADDR, int N>
+__device__ __forceinline__ void load_map(const int64_t* index, int64_t p, int64_t v[N])
+{
+    if (ADDR == kGather) {
+        load_index<N>(index + p, v);
+    } else {
+        const uint4* q = reinterpret_cast<const uint4*>(reinterpret_cast<const uint32_t*>(index) + p);
+#pragma unroll
+        for (int h = 0; h < N / 4; ++h) {
+            const uint4 x = q[h];
+            v[4 * h + 0] = x.x; v[4 * h + 1] = x.y; v[4 * h + 2] = x.z; v[4 * h + 3] = x.w;
+        }
+    }
+}
+
+// Scatter one unit through a map.  When every entry is valid (always, for a
+// partition's own map) the stores run without per-element branches, so they
+// issue back to back: with a branch around each store the wait for the loaded
+// data is repeated before every store and, since stores share the vector
+// memory counter, each store then waits for the one before it.
+template <typename T, int N>
+__device__ __forceinline__ void scatter_unit(T* w, const int64_t idx[N], const T v[N], int64_t numel)
+{
+    uint32_t bad = 0;   // bitwise, not short-circuit: keeps the check free of branches
+#pragma unroll
+    for (int e = 0; e < N; ++e) bad |= (uint64_t)idx[e] >= (uint64_t)numel ? 1u : 0u;
+    if (bad == 0) {
+#pragma unroll
+        for (int e = 0; e < N; ++e) w[idx[e]] = v[e];
+    } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e)
+            if (idx[e] >= 0 && idx[e] < numel) w[idx[e]] = v[e];
+    }
+}
 
 // Resolve the parameter index of position j; returns false for a map entry
 // outside [0, numel) (skipped, never dereferenced).
@@ -116,6 +158,10 @@ __device__ __forceinline__ bool param_at(const int64_t* index, int64_t offset, i
     if (ADDR == kGather) {
         i = index[offset + j];
         return i >= 0 && i < numel;
+    }
+    if (ADDR == kGather32) {
+        i = reinterpret_cast<const uint32_t*>(index)[offset + j];
+        return i < numel;
     }
     const int64_t c = index[offset + (j >> shift)];
     if (c < 0 || c > (numel >> shift)) return false;
@@ -218,15 +264,15 @@ __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
         const int64_t j0 = u * N;
         int64_t base = 0;
         int64_t idx[N];
-        if (ADDR == kGather) {
-            load_index<N>(a.index + a.offset + j0, idx);
+        if (kMap<ADDR>) {
+            load_map<ADDR, N>(a.index, a.offset + j0, idx);
         } else if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
             scalar_body(u);
             return;
         }
         float src[N];
         T old[N];
-        if (ADDR == kGather && AUX != kAuxMaster && AUX != kAuxBackup) {
+        if (kMap<ADDR> && AUX != kAuxMaster && AUX != kAuxBackup) {
 #pragma unroll
             for (int e = 0; e < N; ++e) {
                 const bool ok = idx[e] >= 0 && idx[e] < a.numel;
@@ -252,10 +298,8 @@ __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
         T out[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src[e]));
-        if (ADDR == kGather) {
-#pragma unroll
-            for (int e = 0; e < N; ++e)
-                if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = out[e];
+        if (kMap<ADDR>) {
+            scatter_unit<T, N>(w, idx, out, a.numel);
         } else {
             store_vec<T>(w + base, out);
         }
@@ -284,12 +328,10 @@ __global__ __launch_bounds__(kBlock) void k_restore_copy(StreamArgs a)
         const int64_t j0 = u * N;
         T v[N];
         load_vec<T, NT>(snap + j0, v);
-        if (ADDR == kGather) {
+        if (kMap<ADDR>) {
             int64_t idx[N];
-            load_index<N>(a.index + a.offset + j0, idx);
-#pragma unroll
-            for (int e = 0; e < N; ++e)
-                if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = v[e];
+            load_map<ADDR, N>(a.index, a.offset + j0, idx);
+            scatter_unit<T, N>(w, idx, v, a.numel);
         } else {
             int64_t base;
             if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
@@ -322,9 +364,9 @@ __global__ __launch_bounds__(kBlock) void k_backup_copy(StreamArgs a)
     auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
         T v[N];
-        if (ADDR == kGather) {
+        if (kMap<ADDR>) {
             int64_t idx[N];
-            load_index<N>(a.index + a.offset + j0, idx);
+            load_map<ADDR, N>(a.index, a.offset + j0, idx);
 #pragma unroll
             for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
         } else {
@@ -363,12 +405,10 @@ __global__ __launch_bounds__(kBlock) void k_restore_master(StreamArgs a)
         uint16_t v[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) v[e] = f32_to_bf16(m[e]);
-        if (ADDR == kGather) {
+        if (kMap<ADDR>) {
             int64_t idx[N];
-            load_index<N>(a.index + a.offset + j0, idx);
-#pragma unroll
-            for (int e = 0; e < N; ++e)
-                if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = v[e];
+            load_map<ADDR, N>(a.index, a.offset + j0, idx);
+            scatter_unit<uint16_t, N>(w, idx, v, a.numel);
         } else {
             int64_t base;
             if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
@@ -400,9 +440,9 @@ __global__ __launch_bounds__(kBlock) void k_stage_master(StreamArgs a)
     auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
         T v[N];
-        if (ADDR == kGather) {
+        if (kMap<ADDR>) {
             int64_t idx[N];
-            load_index<N>(a.index + a.offset + j0, idx);
+            load_map<ADDR, N>(a.index, a.offset + j0, idx);
 #pragma unroll
             for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
         } else {
@@ -479,8 +519,8 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
         int64_t idx[N];
         int64_t base = 0;
         T v[N];
-        if (ADDR == kGather) {
-            load_index<N>(a.index + a.offset + j0, idx);
+        if (kMap<ADDR>) {
+            load_map<ADDR, N>(a.index, a.offset + j0, idx);
 #pragma unroll
             for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
         } else {
@@ -504,10 +544,8 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
 #pragma unroll
             for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.step, acc[e], to_f32<T>(v[e])));
         }
-        if (ADDR == kGather) {
-#pragma unroll
-            for (int e = 0; e < N; ++e)
-                if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = out[e];
+        if (kMap<ADDR>) {
+            scatter_unit<T, N>(w, idx, out, a.numel);
         } else {
             store_vec<T>(w + base, out);
         }
@@ -552,7 +590,7 @@ __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
         if (j0 >= len) continue;
         int64_t base = 0;
         const bool vec = ((a.vec_mask >> k) & 1u) && j0 + N <= len &&
-                         (ADDR == kGather || unit_base<ADDR>(a.index, off, a.numel, a.chunk_shift, j0, N, base));
+                         (kMap<ADDR> || unit_base<ADDR>(a.index, off, a.numel, a.chunk_shift, j0, N, base));
         float acc[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) acc[e] = 0.0f;
@@ -567,8 +605,8 @@ __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
         if (vec) {
             T v[N], out[N];
             int64_t idx[N];
-            if (ADDR == kGather) {
-                load_index<N>(a.index + off + j0, idx);
+            if (kMap<ADDR>) {
+                load_map<ADDR, N>(a.index, off + j0, idx);
 #pragma unroll
                 for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
             } else {
@@ -576,10 +614,8 @@ __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
             }
 #pragma unroll
             for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(step, acc[e], to_f32<T>(v[e])));
-            if (ADDR == kGather) {
-#pragma unroll
-                for (int e = 0; e < N; ++e)
-                    if (idx[e] >= 0 && idx[e] < a.numel) w[idx[e]] = out[e];
+            if (kMap<ADDR>) {
+                scatter_unit<T, N>(w, idx, out, a.numel);
             } else {
                 store_vec<T>(w + base, out);
             }
@@ -843,7 +879,12 @@ __global__ __launch_bounds__(kBlock) void k_part_scatter(PartitionArgs a)
             same &= ((b >> bit) & 1u) ? m : ~m;
         }
         const int rank = __popcll(same & below);
-        if (valid) a.index[base[wave][b] + rank] = e;
+        if (valid) {
+            if (a.index32)
+                a.index32[base[wave][b] + rank] = (uint32_t)e;
+            else
+                a.index[base[wave][b] + rank] = e;
+        }
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
         if (valid && rank == 0) base[wave][b] += __popcll(same);
@@ -876,6 +917,37 @@ __global__ __launch_bounds__(kBlock) void k_debug_normals(uint64_t seed, int64_t
             if (j >= j0 && j < j0 + n) out[j - j0] = z[t];
         }
     }
+}
+
+// Seeded normal fill: w[j] = cast(stddev * z_j), z_j the normal of position
+// j in stream (seed, domain).
+template <typename T, bool VEC>
+__global__ __launch_bounds__(kBlock) void k_fill_normal(T* w, int64_t n, uint64_t seed, uint32_t domain, float stddev)
+{
+    constexpr int N = UnitOf<T>::n;
+    const LogEntry* lt = stage_log_table();
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    auto body = [&](int64_t u, bool vec) {
+        const int64_t j0 = u * N;
+        float z[N];
+        if (N == 8)
+            normals8(k0, k1, (uint64_t)j0 >> 2, lt, z, domain);
+        else
+            normals4(k0, k1, (uint64_t)j0 >> 2, lt, z, domain);
+        T v[N];
+#pragma unroll
+        for (int e = 0; e < N; ++e) v[e] = from_f32<T>(stddev * z[e]);
+        if (vec) {
+            store_vec<T>(w + j0, v);
+        } else {
+#pragma unroll
+            for (int e = 0; e < N; ++e)
+                if (j0 + e < n) w[j0 + e] = v[e];
+        }
+    };
+    const int64_t full = n / N;
+    for (int64_t u = global_tid(); u < full; u += grid_stride()) body(u, VEC);
+    if (full * N < n && global_tid() == 0) body(full, false);
 }
 
 __global__ __launch_bounds__(kBlock) void k_debug_bm_grid(uint32_t m0, int64_t n, double* rho, double* c, double* s)
@@ -936,7 +1008,7 @@ int64_t grid_for(int64_t work_items, int64_t cap = kMaxGrid)
 // of the weights (DRAM row and cache locality).
 inline int64_t rng_grid_cap(int addr)
 {
-    return addr == kGather ? kMaxGrid : kRngMaxGrid;
+    return addr == kGather || addr == kGather32 ? kMaxGrid : kRngMaxGrid;
 }
 
 template <typename K, typename A>
@@ -957,6 +1029,8 @@ int64_t units_of(int64_t length)
     switch (addr) {                                                                                  \
     case kGather: return vec ? launch1d(KERNEL<__VA_ARGS__, kGather, true>, u, a, s, cap)                  \
                              : launch1d(KERNEL<__VA_ARGS__, kGather, false>, u, a, s, cap);                \
+    case kGather32: return vec ? launch1d(KERNEL<__VA_ARGS__, kGather32, true>, u, a, s, cap)              \
+                               : launch1d(KERNEL<__VA_ARGS__, kGather32, false>, u, a, s, cap);            \
     case kChunk: return vec ? launch1d(KERNEL<__VA_ARGS__, kChunk, true>, u, a, s, cap)                    \
                             : launch1d(KERNEL<__VA_ARGS__, kChunk, false>, u, a, s, cap);                  \
     default: return vec ? launch1d(KERNEL<__VA_ARGS__, kContig, true>, u, a, s, cap)                       \
@@ -1082,6 +1156,22 @@ hipError_t launch_update(int dtype, bool master, int addr, bool vec, const Updat
 hipError_t launch_update_step(int dtype, int addr, const StepArgs& a, hipStream_t s)
 {
     return dtype == 0 ? update_step_t<uint16_t>(addr, a, s) : update_step_t<float>(addr, a, s);
+}
+
+hipError_t launch_fill_normal(int dtype, void* w, int64_t n, uint64_t seed, uint32_t domain, float stddev, bool vec,
+                              hipStream_t s)
+{
+    const dim3 grid((unsigned)grid_for(n / (dtype == 0 ? 8 : 4) + 1, kRngMaxGrid)), block(kBlock);
+    if (dtype == 0) {
+        uint16_t* p = static_cast<uint16_t*>(w);
+        if (vec) hipLaunchKernelGGL((k_fill_normal<uint16_t, true>), grid, block, 0, s, p, n, seed, domain, stddev);
+        else hipLaunchKernelGGL((k_fill_normal<uint16_t, false>), grid, block, 0, s, p, n, seed, domain, stddev);
+    } else {
+        float* p = static_cast<float*>(w);
+        if (vec) hipLaunchKernelGGL((k_fill_normal<float, true>), grid, block, 0, s, p, n, seed, domain, stddev);
+        else hipLaunchKernelGGL((k_fill_normal<float, false>), grid, block, 0, s, p, n, seed, domain, stddev);
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_normalize(const NormalizeArgs& a, hipStream_t s)

@@ -13,14 +13,15 @@ constexpr int64_t kMaxGrid = 1 << 20;   // workgroups per launch; larger jobs lo
 // LDS per workgroup: a few per CU, each looping over many units.
 constexpr int64_t kRngMaxGrid = 8192;
 
-// Subspace addressing modes (see cpes_subspace).
-enum AddrMode { kAddrContig = 0, kAddrGather = 1, kAddrChunk = 2 };
+// Subspace addressing modes (see cpes_subspace).  kAddrGather32 reads a
+// uint32 map through the same `index` pointer, reinterpreted.
+enum AddrMode { kAddrContig = 0, kAddrGather = 1, kAddrChunk = 2, kAddrGather32 = 3 };
 
 // One subspace operation: positions j in [0, length) at parameter offset + j,
 // index[offset + j], or index[offset + j / 2^s] * 2^s + j mod 2^s (chunks).
 struct StreamArgs {
     void* w;
-    const int64_t* index;   // null: contiguous
+    const int64_t* index;   // null: contiguous; a uint32 map for kAddrGather32
     void* aux;              // snapshot / backup (dtype of w) or fp32 master, may be null
     int64_t offset;
     int64_t length;
@@ -100,7 +101,8 @@ struct PartitionArgs {
     int64_t* pos;           // workspace: exclusive positions, same layout
     int64_t* block_sums;    // workspace: scan block partial sums
     int64_t n_tiles;
-    int64_t* index;         // output map
+    int64_t* index;         // output map (int64), or
+    uint32_t* index32;      // output map (uint32, d <= 2^32)
     int32_t* status;
 };
 
@@ -114,6 +116,8 @@ hipError_t launch_perturb(int dtype, int aux, int addr, bool vec, const StreamAr
 hipError_t launch_restore_copy(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s);
 hipError_t launch_restore_master(int addr, bool vec, const StreamArgs& a, hipStream_t s);
 hipError_t launch_backup_copy(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s);
+hipError_t launch_fill_normal(int dtype, void* w, int64_t n, uint64_t seed, uint32_t domain, float stddev, bool vec,
+                              hipStream_t s);
 hipError_t launch_stage_master(int dtype, int addr, bool vec, const StreamArgs& a, hipStream_t s);
 hipError_t launch_update(int dtype, bool master, int addr, bool vec, const UpdateArgs& a, hipStream_t s);
 hipError_t launch_update_step(int dtype, int addr, const StepArgs& a, hipStream_t s);

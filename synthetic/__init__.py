@@ -164,6 +164,7 @@ class Workload:
     chunk: int = 0                        # chunk size of a chunk-granular partition
     copes_step: bool = False              # members split across all subspaces, one joint update
     host_backup: bool = False             # weight backup in pinned host memory instead of HBM
+    map32: bool = False                   # permutation maps as uint32 (d <= 2^32)
     description: str = ""
 
     @property
@@ -242,6 +243,9 @@ def workload(name: str) -> Workload:
                         scale_mode=SCALE_ALPHA_OVER_N, active=tuple(range(4)), chunk=1 << 16, copes_step=True,
                         description="bf16 4,022,468,096; one CoPES step: K=4 chunk-permuted subspaces, "
                                     "N=40 (10 per subspace), joint z-score, alpha/N_k")
+    if name == "c4u":
+        return dataclasses.replace(workload("c4"), name=name, map32=True,
+                                   description=workload("c4").description + "; uint32 maps")
     if name in ("c3h", "p0h"):
         base = workload(name[:-1])
         return dataclasses.replace(base, name=name, host_backup=True,
@@ -249,4 +253,4 @@ def workload(name: str) -> Workload:
     raise ValueError(name)
 
 
-WORKLOADS = ("c1", "c2", "c3", "c4", "c5", "c4c", "p0", "c3h", "p0h")
+WORKLOADS = ("c1", "c2", "c3", "c4", "c5", "c4c", "p0", "c3h", "p0h", "c4u")

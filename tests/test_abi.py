@@ -37,11 +37,11 @@ def test_header_declares_the_boundary():
 def test_library_exports_every_declared_symbol(lib):
     for name in _declared():
         assert hasattr(lib, name), name
-    assert lib.cpes_abi_version() == 2
+    assert lib.cpes_abi_version() == 3
 
 
-def _sub(offset=0, length=16, index=None):
-    return cp.Subspace(offset, length, index)
+def _sub(offset=0, length=16, index=None, chunk=0, index32=None):
+    return cp.Subspace(offset, length, index, chunk, index32)
 
 
 def _rc_msg(lib, rc):
@@ -99,6 +99,33 @@ def test_host_backup_rejects_bad_arguments(lib):
             assert rc == cp.ERR_INVALID_ARGUMENT, (name, args)
             assert msg.startswith(name + ":"), msg
         assert fn(FAKE, 64, cp.BF16, ctypes.byref(_sub(3, 0)), FAKE, None) == cp.OK   # empty: no-op
+
+
+def test_fill_normal_rejects_bad_arguments(lib):
+    for args in [(FAKE, 16, 7, 1, 1, 0.02),               # bad dtype
+                 (FAKE, -1, cp.BF16, 1, 1, 0.02),         # negative n
+                 (FAKE, 16, cp.BF16, 1, 1, -0.02),        # negative stddev
+                 (FAKE, 16, cp.F32, 1, 1, float("inf")),
+                 (None, 16, cp.F32, 1, 1, 0.02)]:         # null weights
+        rc, msg = _rc_msg(lib, lib.cpes_fill_normal(*args, None))
+        assert rc == cp.ERR_INVALID_ARGUMENT, args
+        assert msg.startswith("cpes_fill_normal:"), msg
+    assert lib.cpes_fill_normal(None, 0, cp.BF16, 1, 1, 0.02, None) == cp.OK
+
+
+def test_uint32_maps_are_validated(lib):
+    both = _sub(0, 16, FAKE, 0, FAKE)                                   # int64 and uint32 map
+    chunked32 = _sub(0, 16, None, 64, FAKE)                             # chunk lists are int64
+    for s in (both, chunked32):
+        rc, msg = _rc_msg(lib, lib.cpes_perturb(FAKE, 64, cp.BF16, ctypes.byref(s), 1e-3, 1, 1, None,
+                                                cp.AUX_NONE, None))
+        assert rc == cp.ERR_INVALID_ARGUMENT and msg.startswith("cpes_perturb:"), msg
+    offs = (ctypes.c_int64 * 9)()
+    assert lib.cpes_partition32((1 << 32) + 1, 8, 1, offs, FAKE, FAKE, 1 << 40, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_partition32(1000, 0, 1, offs, FAKE, FAKE, 1 << 20, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_partition32(1000, 8, 1, offs, None, FAKE, 1 << 20, None, None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_partition32(1000, 8, 1, offs, FAKE, FAKE, 16, None, None) == cp.ERR_WORKSPACE
+    assert lib.cpes_partition32(1000, 300, 1, offs, FAKE, FAKE, 1 << 20, None, None) == cp.ERR_UNSUPPORTED
 
 
 def test_normalize_rejects_bad_arguments(lib):

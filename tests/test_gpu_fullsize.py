@@ -175,7 +175,26 @@ def test_c4_permutation_partition_and_gather(orc, T, big):
         got = _host_bits(w[T.from_numpy(idx_w[p]).cuda()])
         assert bf16_close(got, ref), describe_mismatch(bf16_value(got), bf16_value(ref))
     w.copy_(full_before)
-    del full_before, index
+    # the same partition as a uint32 map (4,022,468,096 < 2^32): identical entries,
+    # and a gather perturbation through it gives the same bits as through the int64 map
+    _say("c4: uint32 map of the same partition")
+    index32 = T.empty(d, dtype=T.int32, device="cuda")
+    ws = T.empty(cp.cpes_partition_workspace_bytes(cp.PART_PERMUTATION, d, K), dtype=T.uint8, device="cuda")
+    offsets32 = cp.cpes_partition32(d, K, W.partition_seed, index32, ws)
+    T.cuda.synchronize()
+    del ws
+    assert offsets32 == offsets
+    for s0 in range(0, d, chunk):
+        assert T.equal(index32[s0:s0 + chunk].to(T.int64) & 0xFFFFFFFF, index[s0:s0 + chunk]), s0
+    cp.cpes_perturb(w, s, sigma, 12, -1)
+    T.cuda.synchronize()
+    via64 = w.clone()
+    w.copy_(full_before)
+    cp.cpes_perturb(w, cp.subspace(off, L, index32), sigma, 12, -1)
+    T.cuda.synchronize()
+    assert T.equal(w, via64)
+    w.copy_(full_before)
+    del full_before, index, index32, via64
 
 
 def test_c5_master_iteration(orc, T, big):

@@ -94,9 +94,27 @@ def test_gpu_normal_statistics(T):
     assert abs(((z - z.mean()) ** 4).mean().item() - 3.0) < 5 * np.sqrt(96.0) * se
 
 
+@pytest.mark.parametrize("dtype", [S.BF16, S.F32])
+@pytest.mark.parametrize("n,shift,seed,domain", [(1, 0, 3, 1), (7, 3, 4, 1), (4095, 1, 5, 0), ((1 << 20) + 5, 3, 6, 7)])
+def test_fill_normal_matches_oracle(orc, T, dtype, n, shift, seed, domain):
+    """Seeded fill against the oracle's, at an aligned or unaligned start."""
+    tdt = T.bfloat16 if dtype == S.BF16 else T.float32
+    buf = T.zeros(n + shift, dtype=tdt, device="cuda")
+    w = buf[shift:]
+    cp.cpes_fill_normal(w, seed, domain, 0.02)
+    _sync(T)
+    got = to_host(w)
+    ref = orc.fill_normal(n, dtype, seed, domain, 0.02)
+    if dtype == S.BF16:
+        assert ulp_bf16(got, ref).max() <= 1
+    else:
+        assert ulp_f32(got, ref).max() <= 3
+    assert not to_host(buf[:shift]).any()                       # nothing written before the start
+
+
 # ------------------------------------------------------------ perturb etc --
 
-LAYOUTS = ["aligned", "unaligned", "gather", "chunked"]
+LAYOUTS = ["aligned", "unaligned", "gather", "gather_v", "gather32", "chunked"]
 CHUNK = 64
 LENGTHS = [1, 7, 9, 4095, (1 << 20) + 5]
 
@@ -117,17 +135,20 @@ def _chunk_partition(d):
 
 def _layout(layout, length):
     """(numel, offset, host index map or None) for a subspace of `length`:
-    a contiguous range at an aligned or unaligned offset, or subspace 1 of a
-    4-way permutation partition of 4 * length indices (its map starts at an
-    offset that is not a multiple of the vector width)."""
+    a contiguous range at an aligned or unaligned offset, or a subspace of a
+    4-way permutation partition of 4 * length indices: subspace 1 ("gather",
+    its map starts at an odd entry, so units take the element path) or
+    subspace 0 ("gather_v", "gather32": 16-byte map vectors; gather32 passes
+    the map as uint32)."""
     if layout == "aligned":
         return length + 64, 16, None
     if layout == "unaligned":
         return length + 64, 3, None
     d = max(4 * length, 8)
     offsets, index = _perm_partition(d)
-    assert offsets[2] - offsets[1] >= length
-    return d, int(offsets[1]), index
+    k = 1 if layout == "gather" else 0
+    assert offsets[k + 1] - offsets[k] >= length
+    return d, int(offsets[k]), index
 
 
 def _setup(orc, T, dtype, layout, length, wseed):
@@ -145,7 +166,11 @@ def _setup(orc, T, dtype, layout, length, wseed):
         return w, to_dev(w), 0, index, sub
     numel, offset, index = _layout(layout, length)
     w = S.host_weights(numel, dtype, wseed)
-    return w, to_dev(w), offset, index, cp.subspace(offset, length, to_dev(index) if index is not None else None)
+    if layout == "gather32":
+        dev_map = to_dev(index.astype(np.uint32).view(np.int32))
+    else:
+        dev_map = to_dev(index) if index is not None else None
+    return w, to_dev(w), offset, index, cp.subspace(offset, length, dev_map)
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
@@ -404,6 +429,17 @@ def test_permutation_partition_bit_exact(orc, T, d, K):
     assert offsets == [int(x) for x in ref_off]
     assert int(st.item()) == 0
     assert np.array_equal(to_host(index), ref_index)
+
+
+@pytest.mark.parametrize("d,K", [(1, 1), (7, 3), (100003, 8), ((1 << 20) + 3, 256)])
+def test_permutation_partition32_bit_exact(orc, T, d, K):
+    ws = T.empty(cp.cpes_partition_workspace_bytes(cp.PART_PERMUTATION, d, K), dtype=T.uint8, device="cuda")
+    index = T.full((d,), -1, dtype=T.int32, device="cuda")
+    offsets = cp.cpes_partition32(d, K, 33, index, ws)
+    ref_off, ref_index = orc.partition(orc.PART_PERMUTATION, d, K, seed=33)
+    _sync(T)
+    assert offsets == [int(x) for x in ref_off]
+    assert np.array_equal(to_host(index).view(np.uint32).astype(np.int64), ref_index)
 
 
 def test_prp_values_bit_exact(orc, T):

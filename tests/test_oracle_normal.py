@@ -158,3 +158,40 @@ def test_normal_window_is_prefix_free(orc):
     for j0 in (0, 1, 3, 4, 7, 1001, 4000):
         assert np.array_equal(orc.normals(9, j0, 4096 - j0), full[j0:])
     assert orc.normal(9, 2**40 + 3) == orc.normals(9, 2**40, 8)[3]
+
+
+# ------------------------------------------------------ seeded normal fill --
+
+def test_fill_normal_reduces_to_the_pinned_noise(orc):
+    """Unit scale in fp32 returns the normals themselves: domain 0 is the
+    perturbation noise pinned above, and other domains use the same
+    transform on their own Philox words."""
+    n = 4099
+    assert np.array_equal(orc.fill_normal(n, orc.F32, 5, 0, 1.0), orc.normals(5, 0, n))
+    for j in (0, 1, 2, 3, 4, 1000, n - 1):
+        x = orc.blocks(5, 1, j // 4, 1)
+        a, b = (x[0], x[1]) if j % 4 < 2 else (x[2], x[3])
+        c, s = orc.bm_angle(int(b))
+        ref = np.float32(orc.bm_radius(int(a)) * (s if j % 2 else c))
+        assert orc.fill_normal(n, orc.F32, 5, 1, 1.0)[j] == ref
+        assert orc.normal_domain(5, 1, j) == ref
+
+
+def test_fill_normal_scale_rounding_and_zero(orc):
+    n = 10000
+    z = orc.fill_normal(n, orc.F32, 9, 1, 1.0)
+    f = orc.fill_normal(n, orc.F32, 9, 1, 0.02)
+    assert np.array_equal(f, (np.float32(0.02) * z).astype(np.float32))          # one fp32 multiply
+    h = orc.fill_normal(n, orc.BF16, 9, 1, 0.02)
+    assert np.array_equal(h, np.array([orc.f32_to_bf16(float(v)) for v in f], dtype=np.uint16))
+    assert not np.any(orc.fill_normal(n, orc.F32, 9, 1, 0.0))
+
+
+def test_fill_normal_statistics_and_domain_separation(orc):
+    n = 1 << 20
+    w = orc.fill_normal(n, orc.F32, 0, 1, 0.02).astype(np.float64)
+    se = 0.02 / math.sqrt(n)
+    assert abs(w.mean()) < 5 * se
+    assert abs(w.std() - 0.02) < 5 * 0.02 / math.sqrt(2 * n)
+    noise = orc.normals(0, 0, n).astype(np.float64)
+    assert abs(np.corrcoef(w, noise)[0, 1]) < 5 / math.sqrt(n)                    # domains are independent
