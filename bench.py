@@ -51,12 +51,22 @@ def parse():
     p.add_argument("--warmup", type=int, default=1)
     p.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c4c", "p0", "c3h", "p0h", "c4u"])
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-graph", action="store_true",
+                   help="skip the HIP-graph timing (by default one step is also captured in a graph and K replays "
+                        "of it are timed: graph_ms_per_step)")
     p.add_argument("--kernels-once", action="store_true",
                    help="run each kernel once on one 504,654,080-position subspace (for counter passes) and exit")
     p.add_argument("--cpu-positions", type=int, default=None,
                    help="positions per subspace sample for the oracle baseline (default: 2^31 / members, "
                         "about 10-30 s of host work)")
     return p.parse_args()
+
+
+class NoTimer:
+    """Stands in for KernelTimer inside graph capture (no events)."""
+
+    def run(self, name, fn, positions=0):
+        fn()
 
 
 class KernelTimer:
@@ -225,6 +235,24 @@ def bytes_per_position(W, op):
     return 0
 
 
+def graph_step_ms(W, cp, torch, P, cache, steps):
+    """One step captured in a HIP graph (torch.cuda.CUDAGraph), then `steps`
+    replays timed between synchronisations: the step without per-launch host
+    overhead.  The library only enqueues kernels, so the step captures whole."""
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run_step(W, cp, torch, P, NoTimer(), cache)
+    g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.replay()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    del g
+    return ms
+
+
 def copy_reference(W, torch, P, sizes):
     """The achievable-HBM reference, in the same run: torch's device-to-device
     copy (hipMemcpy) of the largest subspace's weights, median of 5."""
@@ -371,6 +399,8 @@ def main():
     elapsed = time.perf_counter() - t0
     timer.collect()
     ms_step = elapsed * 1e3 / args.steps
+    # host-backup steps query pointer attributes while enqueueing, which stream capture does not allow
+    graph_ms = None if (args.no_graph or W.host_backup) else graph_step_ms(W, cp, torch, P, cache, args.steps)
 
     sizes = [n for _, n in cache["parts"]] if "parts" in cache else W.sizes()
     span = sum(sizes[k] for k in W.active)                # subspace positions visited per step
@@ -447,6 +477,8 @@ def main():
     if part_ms is not None:
         line["partition_ms"] = round(part_ms, 3)
     line["copy_reference"] = copy_reference(W, torch, P, sizes)
+    if graph_ms is not None:
+        line["graph_ms_per_step"] = round(graph_ms, 3)
     if not args.no_cpu_baseline:
         positions = args.cpu_positions or (1 << 31) // W.n
         line["cpu_baseline"] = cpu_baseline(W, positions)
