@@ -1,12 +1,13 @@
 // cpes_kernels.hip -- gfx950 kernels of the CoPES parameter-space hot path.
 //
-// Streaming kernels (perturb, restore, master staging, update) give every
-// thread one "unit" of consecutive subspace positions: 8 for bf16 weights
-// (one 16-byte vector, two Philox blocks) and 4 for fp32 weights (one 16-byte
-// vector, one Philox block).  A wave therefore moves 1 KiB per vector access,
-// fully coalesced.  Units whose 16-byte vectors are not aligned (an odd
-// subspace offset) and the ragged tail take an element-by-element path with
-// the same arithmetic.  Noise never leaves registers.
+// Streaming kernels (perturb, restore, master staging, update) work on
+// "units" of consecutive subspace positions: 8 for bf16 weights (one 16-byte
+// vector, two Philox blocks) and 4 for fp32 weights (one 16-byte vector, one
+// Philox block), one unit per thread at a time.  A wave therefore moves 1 KiB
+// per vector access, fully coalesced.  Units whose 16-byte vectors are not
+// aligned (an odd subspace offset, an odd map entry) and the ragged tail take
+// an element-by-element path with the same arithmetic.  Subspaces are ranges,
+// int64 or uint32 element maps, or chunk lists.  Noise never leaves registers.
 #include "cpes_device.hpp"
 #include "cpes_launch.hpp"
 
