@@ -51,6 +51,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=1)
     p.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c4c", "p0", "c3h", "p0h", "c4u"])
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--fused-restore", action="store_true",
+                   help="variant schedule, reported separately from the headline: members after the first perturb "
+                        "from the backup (restore and perturbation in one pass) and one restore follows the last")
     p.add_argument("--no-graph", action="store_true",
                    help="skip the HIP-graph timing (by default one step is also captured in a graph and K replays "
                         "of it are timed: graph_ms_per_step)")
@@ -146,7 +149,7 @@ def random_partition(W, cp, P):
     return [(offs[k], lens[k]) for k in range(W.K)]
 
 
-def run_step(W, cp, torch, P, timer, cache):
+def run_step(W, cp, torch, P, timer, cache, fused=False):
     """One pass of the hot path over the workload."""
     import synthetic as S
 
@@ -180,10 +183,13 @@ def run_step(W, cp, torch, P, timer, cache):
             # restored weights in place, or, on an index map, read the (contiguous)
             # backup instead of gathering w (a master source is read by every member)
             mode = aux_mode if (W.master or m == 0) else later
+            if fused and m > 0 and not W.master:
+                mode = cp.AUX_BACKUP                 # restore of the previous member + perturbation, one pass
             timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigmas[k], seed, sign, aux=aux, aux_mode=mode),
                       n_k)
             # (the perturbed model would be evaluated here)
-            timer.run("restore", lambda: cp.cpes_restore(P["w"], s, aux=aux, aux_mode=aux_mode), n_k)
+            if not fused or m == len(seeds) - 1:
+                timer.run("restore", lambda: cp.cpes_restore(P["w"], s, aux=aux, aux_mode=aux_mode), n_k)
 
     if W.copes_step:
         # Alg. 1: every subspace gets N/K members, joint standardisation, one composed update
@@ -235,13 +241,13 @@ def bytes_per_position(W, op):
     return 0
 
 
-def graph_step_ms(W, cp, torch, P, cache, steps):
+def graph_step_ms(W, cp, torch, P, cache, steps, fused=False):
     """One step captured in a HIP graph (torch.cuda.CUDAGraph), then `steps`
     replays timed between synchronisations: the step without per-launch host
     overhead.  The library only enqueues kernels, so the step captures whole."""
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        run_step(W, cp, torch, P, NoTimer(), cache)
+        run_step(W, cp, torch, P, NoTimer(), cache, fused)
     g.replay()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -389,18 +395,18 @@ def main():
         part_ms = e0.elapsed_time(e1)
     warm = KernelTimer(torch)
     for _ in range(args.warmup):
-        run_step(W, cp, torch, P, warm, cache)
+        run_step(W, cp, torch, P, warm, cache, args.fused_restore)
     torch.cuda.synchronize()
     timer = KernelTimer(torch)
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        run_step(W, cp, torch, P, timer, cache)
+        run_step(W, cp, torch, P, timer, cache, args.fused_restore)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     timer.collect()
     ms_step = elapsed * 1e3 / args.steps
     # host-backup steps query pointer attributes while enqueueing, which stream capture does not allow
-    graph_ms = None if (args.no_graph or W.host_backup) else graph_step_ms(W, cp, torch, P, cache, args.steps)
+    graph_ms = None if (args.no_graph or W.host_backup) else graph_step_ms(W, cp, torch, P, cache, args.steps, args.fused_restore)
 
     sizes = [n for _, n in cache["parts"]] if "parts" in cache else W.sizes()
     span = sum(sizes[k] for k in W.active)                # subspace positions visited per step
@@ -410,7 +416,8 @@ def main():
         avg_ms, count, tot_ms = timer.stats(op)
         if count == 0:
             continue
-        per_step = span * (per_sub_members if op in ("perturb", "restore", "restore_host") else 1)
+        reps = per_sub_members if op in ("perturb", "restore_host") or (op == "restore" and not args.fused_restore) else 1
+        per_step = span * reps
         per_launch = per_step / (count / args.steps)     # average positions per launch
         entry = {"launches": count, "avg_ms": round(avg_ms, 4), "ms_per_step": round(tot_ms / args.steps, 3),
                  "positions_per_launch": round(per_launch)}
@@ -470,7 +477,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{W.name}: {W.description}", "d": W.d, "K": W.K, "members": W.n,
                    "active_subspaces": len(W.active), "weights": "bf16" if W.dtype == S.BF16 else "f32",
-                   "noise": "Philox4x32-10 + fp64 Box-Muller, fp32 FMA"},
+                   "noise": "Philox4x32-10 + fp64 Box-Muller, fp32 FMA",
+                   "schedule": ("fused restore (variant): one pass restores and perturbs each later member"
+                                if args.fused_restore else "perturb and restore per member")},
         "roofline": roof,
         "ops": ops,
     }
