@@ -140,8 +140,11 @@ struct AngleParts {
 
 __device__ __forceinline__ AngleParts bm_angle_parts(uint32_t b)
 {
-    const uint32_t m = (b >> 8) + 1u;
-    const uint32_t rem = m & 0x3FFFFFu;
+    // s8 = (m << 8) mod 2^32, m = (b >> 8) + 1: adding 0x100 to b cannot carry
+    // out of its low byte, so bits 8..31 of s8 are m's bits 0..23 (m = 2^24
+    // wraps to 0, the same angle); bit 31 of s8 is then the sign of sin theta.
+    const uint32_t s8 = b + 0x100u;
+    const uint32_t rem = (s8 >> 8) & 0x3FFFFFu;             // m mod 2^22
     const bool fold = rem > (1u << 21);
     const double t = (double)(fold ? (1u << 22) - rem : rem);
     const double t2 = t * t;
@@ -161,9 +164,9 @@ __device__ __forceinline__ AngleParts bm_angle_parts(uint32_t b)
     AngleParts r;
     r.sp = sp;
     r.cp = cp;
-    r.take_sin = fold ^ (((m >> 22) & 1u) != 0u);           // odd quadrant swaps the roles
-    r.cos_sign = (m + (1u << 22)) << 8;                     // bit 31: quadrant 1 or 2
-    r.sin_sign = m << 8;                                    // bit 31: quadrant 2 or 3
+    r.take_sin = fold ^ (((s8 >> 30) & 1u) != 0u);          // odd quadrant (bit 22 of m) swaps the roles
+    r.cos_sign = s8 + 0x40000000u;                          // bit 31: quadrant 1 or 2
+    r.sin_sign = s8;                                        // bit 31: quadrant 2 or 3
     return r;
 }
 
