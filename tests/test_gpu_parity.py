@@ -367,6 +367,7 @@ MEMBER_SETS = {
     "pairs4": ([9, 9, 12, 40], [1, -1, 1, 1]),
     "n30": (list(range(1, 31)), [1] * 30),
     "n128_antithetic": ([s for s in range(1001, 1065) for _ in (0, 1)], [1, -1] * 64),
+    "n256_max": (list(range(2001, 2257)), [1, -1] * 128),             # CPES_MAX_MEMBERS distinct streams
 }
 
 
@@ -411,6 +412,22 @@ def test_update_mirrored_equal_rewards_is_identity(T):
     dw = to_dev(w)
     rn = to_dev(np.array([0.7, 0.7, -1.1, -1.1], np.float32))
     cp.cpes_update(dw, cp.subspace(0, 100003), [4, 4, 8, 8], [1, -1, 1, -1], rn, 5e-4, 4e-3)
+    _sync(T)
+    assert np.array_equal(to_host(dw), w)
+
+
+@pytest.mark.parametrize("dtype", [S.BF16, S.F32])
+def test_degenerate_calls_leave_weights_untouched(T, dtype):
+    """sigma = 0 perturbs to the same bits (one fp32 FMA with a zero product,
+    then the exact bf16 rounding of an exact value), an empty subspace and a
+    zero step do nothing."""
+    w = S.host_weights(70001, dtype, 12)
+    dw = to_dev(w)
+    s = cp.subspace(1, 70000)
+    cp.cpes_perturb(dw, s, 0.0, 3, 1)
+    cp.cpes_perturb(dw, cp.subspace(9, 0), 1e-2, 3, 1)
+    cp.cpes_update(dw, s, [1, 2], [1, 1], to_dev(np.array([0.3, -0.3], np.float32)), 0.0, 1e-3)
+    cp.cpes_restore(dw, cp.subspace(70001, 0), aux=None, aux_mode=cp.AUX_NONE, sigma=1e-3)
     _sync(T)
     assert np.array_equal(to_host(dw), w)
 
