@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define CPES_ABI_VERSION 3
+#define CPES_ABI_VERSION 4
 
 /* Exported symbols (the library is built with hidden default visibility). */
 #define CPES_API __attribute__((visibility("default")))
@@ -92,6 +92,11 @@ typedef struct cpes_subspace {
     const uint32_t* index32; /* NULL, or device uint32 map of parameters (half the map traffic
                                 of `index`; models of at most 2^32 parameters); at most one of
                                 index / index32, and chunk = 0 with index32 */
+    int64_t noise_offset;    /* 0, or a multiple of 8: position j draws noise index
+                                noise_offset + j.  A shard [a, b) of a subspace is
+                                {offset + a (or the map entry a), b - a, ..., noise_offset = a}
+                                and gets exactly the noise, and the results, of those positions
+                                of the whole subspace (a sharded update across GPUs). */
 } cpes_subspace;
 
 /*

@@ -40,7 +40,7 @@ class CpesError(RuntimeError):
 
 class Subspace(ctypes.Structure):
     _fields_ = [("offset", ctypes.c_int64), ("length", ctypes.c_int64), ("index", ctypes.c_void_p),
-                ("chunk", ctypes.c_int64), ("index32", ctypes.c_void_p)]
+                ("chunk", ctypes.c_int64), ("index32", ctypes.c_void_p), ("noise_offset", ctypes.c_int64)]
 
 
 _lib = None
@@ -149,11 +149,12 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
-def subspace(offset: int, length: int, index=None, chunk: int = 0) -> Subspace:
+def subspace(offset: int, length: int, index=None, chunk: int = 0, noise_offset: int = 0) -> Subspace:
     """Positions j < length at parameter offset + j, index[offset + j], or
     (chunk > 0) index[offset + j // chunk] * chunk + j % chunk.  An int64 map
     goes to ``index``; a 32-bit map (torch.int32 or torch.uint32 holding the
-    uint32 entries of cpes_partition32) goes to ``index32``."""
+    uint32 entries of cpes_partition32) goes to ``index32``.  Position j uses
+    noise index noise_offset + j (a shard of a larger subspace)."""
     torch = _torch()
     idx64 = idx32 = None
     if index is not None:
@@ -163,7 +164,7 @@ def subspace(offset: int, length: int, index=None, chunk: int = 0) -> Subspace:
             idx32 = _dev_ptr(index, "index map")
         else:
             raise TypeError("index map must be int64, or 32-bit for a uint32 map")
-    sub = Subspace(int(offset), int(length), idx64, int(chunk), idx32)
+    sub = Subspace(int(offset), int(length), idx64, int(chunk), idx32, int(noise_offset))
     sub._index = index      # the descriptor holds a raw pointer: keep the map's storage alive with it
     return sub
 

@@ -55,6 +55,9 @@ int check_subspace(const void* w, int64_t numel, int dtype, const cpes_subspace*
                     (long long)s->length);
     if (s->length > (INT64_MAX / 8) - s->offset)
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: offset + length overflows", fn);
+    if (s->noise_offset < 0 || (s->noise_offset & 7) != 0 || s->noise_offset > (INT64_MAX / 8) - s->length)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: noise_offset %lld is negative, not a multiple of 8 or too large",
+                    fn, (long long)s->noise_offset);
     if (s->index && s->index32)
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: a subspace takes an int64 or a uint32 map, not both", fn);
     if (s->index32 && s->chunk != 0)
@@ -130,6 +133,7 @@ cpes::StreamArgs stream_args(void* w, int64_t numel, const cpes_subspace* s, con
     a.k1 = (uint32_t)(seed >> 32);
     a.scale = scale;
     a.chunk_shift = s->chunk ? log2_exact(s->chunk) : 0;
+    a.noise0 = s->noise_offset;
     return a;
 }
 
@@ -527,6 +531,7 @@ int cpes_update(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, f
     a.n_members = n;
     a.n_streams = n_streams;
     a.chunk_shift = s->chunk ? log2_exact(s->chunk) : 0;
+    a.noise0 = s->noise_offset;
     const bool vec = vector_ok(w_dev, dtype, s, master_dev, true);
     return hip_status(cpes::launch_update(dtype, master_dev != nullptr, addr_mode(s), vec, a, (hipStream_t)stream), fn);
 }

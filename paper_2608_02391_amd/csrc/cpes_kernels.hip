@@ -242,7 +242,7 @@ __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
     auto scalar_body = [&](int64_t u) {
         const int64_t j0 = u * N;
         float z[N];
-        unit_normals<N>(a.k0, a.k1, (uint64_t)j0 >> 2, lt, z);
+        unit_normals<N>(a.k0, a.k1, (uint64_t)(a.noise0 + j0) >> 2, lt, z);
 #pragma unroll
         for (int e = 0; e < N; ++e) {
             const int64_t j = j0 + e;
@@ -295,7 +295,7 @@ __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
             if (AUX == kAuxSnapshot) store_vec<T>(static_cast<T*>(a.aux) + j0, old);
         }
         float z[N];
-        unit_normals<N>(a.k0, a.k1, (uint64_t)j0 >> 2, lt, z);
+        unit_normals<N>(a.k0, a.k1, (uint64_t)(a.noise0 + j0) >> 2, lt, z);
         T out[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src[e]));
@@ -488,7 +488,7 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
         for (int s = 0; s < a.n_streams; ++s) {
             const float c = coef[s];
             float z[N];
-            unit_normals<N>(a.seed_lo[s], a.seed_hi[s], (uint64_t)j0 >> 2, lt, z);
+            unit_normals<N>(a.seed_lo[s], a.seed_hi[s], (uint64_t)(a.noise0 + j0) >> 2, lt, z);
 #pragma unroll
             for (int e = 0; e < N; ++e) acc[e] = __builtin_fmaf(c, z[e], acc[e]);
         }

@@ -29,6 +29,7 @@ struct StreamArgs {
     uint32_t k0, k1;        // Philox key = member seed
     float scale;            // +-sigma applied to the noise
     int32_t chunk_shift;    // s for chunked subspaces
+    int64_t noise0;         // noise index of position 0 (a shard of a larger subspace)
 };
 
 enum AuxKind { kAuxNone = 0, kAuxSnapshot = 1, kAuxMaster = 2, kAuxBackup = 3 };
@@ -49,6 +50,7 @@ struct UpdateArgs {
     int32_t n_members;
     int32_t n_streams;
     int32_t chunk_shift;
+    int64_t noise0;         // noise index of position 0
     uint32_t seed_lo[kMaxMembers];
     uint32_t seed_hi[kMaxMembers];
     uint8_t member_stream[kMaxMembers];

@@ -37,11 +37,11 @@ def test_header_declares_the_boundary():
 def test_library_exports_every_declared_symbol(lib):
     for name in _declared():
         assert hasattr(lib, name), name
-    assert lib.cpes_abi_version() == 3
+    assert lib.cpes_abi_version() == 4
 
 
-def _sub(offset=0, length=16, index=None, chunk=0, index32=None):
-    return cp.Subspace(offset, length, index, chunk, index32)
+def _sub(offset=0, length=16, index=None, chunk=0, index32=None, noise_offset=0):
+    return cp.Subspace(offset, length, index, chunk, index32, noise_offset)
 
 
 def _rc_msg(lib, rc):
@@ -63,6 +63,8 @@ def test_perturb_rejects_bad_arguments(lib):
         (FAKE, 8, cp.BF16, ctypes.byref(s), 1e-3, 1, 1, None, cp.AUX_NONE),         # beyond numel
         (FAKE, 64, cp.BF16, ctypes.byref(_sub(0, -1)), 1e-3, 1, 1, None, cp.AUX_NONE),
         (FAKE, 64, cp.BF16, ctypes.byref(_sub(-4, 4)), 1e-3, 1, 1, None, cp.AUX_NONE),
+        (FAKE, 64, cp.BF16, ctypes.byref(_sub(0, 16, noise_offset=-8)), 1e-3, 1, 1, None, cp.AUX_NONE),
+        (FAKE, 64, cp.BF16, ctypes.byref(_sub(0, 16, noise_offset=12)), 1e-3, 1, 1, None, cp.AUX_NONE),  # not 8k
     ]
     for args in cases:
         rc, msg = _rc_msg(lib, lib.cpes_perturb(*args, None))
