@@ -114,8 +114,9 @@ def test_fill_normal_matches_oracle(orc, T, dtype, n, shift, seed, domain):
 
 # ------------------------------------------------------------ perturb etc --
 
-LAYOUTS = ["aligned", "unaligned", "gather", "gather_v", "gather32", "chunked"]
-CHUNK = 64
+LAYOUTS = ["aligned", "unaligned", "gather", "gather_v", "gather32", "chunked", "chunked_wave"]
+CHUNK = 64              # chunks shorter than a wave's 64 units: per-lane chunk ids
+CHUNK_WAVE = 1024       # a wave's units share a chunk (64 x 8 bf16 or 64 x 4 fp32 positions): one scalar id
 LENGTHS = [1, 7, 9, 4095, (1 << 20) + 5]
 
 
@@ -127,10 +128,10 @@ def _perm_partition(d):
 
 
 @functools.lru_cache(maxsize=None)
-def _chunk_partition(d):
+def _chunk_partition(d, chunk=CHUNK):
     import oracle as O
 
-    return O.partition_chunks(d, CHUNK, 4, 33)
+    return O.partition_chunks(d, chunk, 4, 33)
 
 
 def _layout(layout, length):
@@ -154,15 +155,17 @@ def _layout(layout, length):
 def _setup(orc, T, dtype, layout, length, wseed):
     """Host weights, device weights, host (offset, element map) for the oracle,
     and the device subspace.  A chunked subspace is subspace 1 of a 4-way
-    chunk partition (chunk 64): the device gets its chunk list, the oracle the
-    element map the chunk list expands to."""
-    if layout == "chunked":
-        d = 4 * (length + 2 * CHUNK)
-        offs, lens, chunks = _chunk_partition(d)
+    chunk partition (chunks of 64, or of 1,024 so that a wave shares one chunk
+    id): the device gets its chunk list, the oracle the element map the chunk
+    list expands to."""
+    if layout in ("chunked", "chunked_wave"):
+        C = CHUNK if layout == "chunked" else CHUNK_WAVE
+        d = 4 * (length + 2 * C)
+        offs, lens, chunks = _chunk_partition(d, C)
         assert lens[1] >= length
         w = S.host_weights(d, dtype, wseed)
-        index = orc.expand_chunks(chunks, int(offs[1]), length, CHUNK)
-        sub = cp.subspace(int(offs[1]), length, to_dev(chunks), CHUNK)
+        index = orc.expand_chunks(chunks, int(offs[1]), length, C)
+        sub = cp.subspace(int(offs[1]), length, to_dev(chunks), C)
         return w, to_dev(w), 0, index, sub
     numel, offset, index = _layout(layout, length)
     w = S.host_weights(numel, dtype, wseed)
