@@ -363,6 +363,19 @@ def test_normalize_grouped_and_failures(orc, T, mode):
     assert np.all(to_host(out) == 0) and int(st.item()) == 2
 
 
+def test_normalize_at_the_limits(orc, T):
+    """4096 rewards (CPES_MAX_REWARDS) in 1024 groups (CPES_MAX_GROUPS) of 4."""
+    n, K = 4096, 1024
+    for mode in (S.NORM_Z, S.NORM_RANK):
+        r = S.rewards("mean_bernoulli", n, 31)
+        g = (np.arange(n) % K).astype(np.int32)
+        out = T.empty(n, dtype=T.float32, device="cuda")
+        cp.cpes_normalize_rewards(to_dev(r), out, mode, group=to_dev(g), n_groups=K)
+        ref, st = orc.normalize(r, mode, g)
+        _sync(T)
+        assert st == 0 and np.array_equal(to_host(out), ref)
+
+
 # ------------------------------------------------------------------ update --
 
 MEMBER_SETS = {
@@ -485,6 +498,8 @@ STEP_CASES = {
     "contig_unaligned": (300007, 3, [0, 1001, 150003, 300007], [5, 3, 4]),
     "contig_k1_std_es": (262147, 1, "equal", [8]),
     "contig_k8_empty": ((1 << 19) + 64, 8, "equal", [2, 0, 3, 1, 1, 0, 2, 2]),
+    "contig_k32_n256_max": ((1 << 20) + 7, 32, "equal", [8] * 32),       # CPES_MAX_STEP_SUBSPACES, CPES_MAX_MEMBERS
+    "chunk1024_k4": ((1 << 20) + 3, 4, "chunk1024", [6, 7, 8, 9]),      # a wave shares one chunk id
 }
 
 
@@ -495,8 +510,8 @@ def test_update_step_matches_oracle(orc, T, case, dtype, scale):
     d, K, part, per = STEP_CASES[case]
     index = dindex = lengths = None
     chunk = 0
-    if part == "chunk":
-        chunk = 256
+    if part in ("chunk", "chunk1024"):
+        chunk = 256 if part == "chunk" else 1024
         offsets, lengths, chunks = orc.partition_chunks(d, chunk, K, 33)
         dindex = to_dev(chunks)
         # the oracle sees each chunked subspace through its element map, laid end to end
@@ -511,7 +526,7 @@ def test_update_step_matches_oracle(orc, T, case, dtype, scale):
     else:
         offsets = np.array(part, dtype=np.int64)
     offsets = [int(x) for x in offsets]
-    if part != "chunk":
+    if part not in ("chunk", "chunk1024"):
         host_offsets = offsets
     subs = [k for k in range(K) for _ in range(per[k])]
     n = len(subs)
