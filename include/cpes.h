@@ -36,15 +36,18 @@
  *                                               (index != NULL, chunk > 0:
  *                                                the map names chunks of `chunk`
  *                                                consecutive parameters),
- * index being a device array of int64.  Entries that would address outside
- * [0, numel) are skipped.
+ * index being a device array of int64; an element map may instead be a
+ * uint32 array (index32, models of at most 2^32 parameters).  Entries that
+ * would address outside [0, numel) are skipped.
  *
- * Noise.  Position j of the noise of a member with seed s is
- *   eps_j = BoxMuller(Philox4x32-10(counter = (lo32 q, hi32 q, 0, 0),
- *                                   key = (lo32 s, hi32 s)), j mod 4),
- * q = j / 4: words (x0, x1) give positions 4q and 4q+1, words (x2, x3) give
+ * Noise.  Position j of a subspace draws noise index i = noise_offset + j
+ * (noise_offset = 0 for a whole subspace; a shard of one passes its start).
+ * Noise index i of a member with seed s is
+ *   eps_i = BoxMuller(Philox4x32-10(counter = (lo32 q, hi32 q, 0, 0),
+ *                                   key = (lo32 s, hi32 s)), i mod 4),
+ * q = i / 4: words (x0, x1) give indices 4q and 4q+1, words (x2, x3) give
  * 4q+2 and 4q+3; radius sqrt(-2 ln U(a)), angle 2 pi U(b), U(x) = ((x >> 8) +
- * 1) 2^-24; cosine for the even position, sine for the odd one; evaluated in
+ * 1) 2^-24; cosine for the even index, sine for the odd one; evaluated in
  * fp64 and rounded once to fp32.
  */
 #ifndef CPES_H
