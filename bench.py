@@ -35,10 +35,10 @@ VALU_LANE_OPS_PEAK = 256 * 64 * 2.4e9  # 256 CUs x 64 lanes x 2.4 GHz: one VALU 
 # size reads).  Valid for the kernels as profiled; re-measure after a kernel
 # change.
 MEASURED = {
-    "perturb": {"valu_per_normal": 38.5, "hbm_bytes_first": 6.0, "hbm_bytes_rest": 4.0},
-    "perturb_master": {"valu_per_normal": 37.6, "hbm_bytes": 6.0},
-    "update": {"valu_per_normal": 36.0, "hbm_bytes": 4.0},
-    "update_master": {"valu_per_normal": 36.0, "hbm_bytes": 10.0},
+    "perturb": {"valu_per_normal": 33.8, "hbm_bytes_first": 6.0, "hbm_bytes_rest": 4.0},
+    "perturb_master": {"valu_per_normal": 33.6, "hbm_bytes": 6.0},
+    "update": {"valu_per_normal": 31.3, "hbm_bytes": 4.0},
+    "update_master": {"valu_per_normal": 31.2, "hbm_bytes": 10.0},
     "restore": {"hbm_bytes": 4.0},
     "restore_master": {"hbm_bytes": 6.0},
 }

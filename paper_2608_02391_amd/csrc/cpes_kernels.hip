@@ -28,16 +28,16 @@ template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) { re
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 
 template <int N>
-__device__ __forceinline__ void unit_normals(uint32_t k0, uint32_t k1, uint64_t q, const LogEntry* lt, float z[N]);
+__device__ __forceinline__ void unit_normals(uint32_t k0, uint32_t k1, uint64_t q, const BmTables* tb, float z[N]);
 template <>
-__device__ __forceinline__ void unit_normals<4>(uint32_t k0, uint32_t k1, uint64_t q, const LogEntry* lt, float z[4])
+__device__ __forceinline__ void unit_normals<4>(uint32_t k0, uint32_t k1, uint64_t q, const BmTables* tb, float z[4])
 {
-    normals4(k0, k1, q, lt, z);
+    normals4(k0, k1, q, tb, z);
 }
 template <>
-__device__ __forceinline__ void unit_normals<8>(uint32_t k0, uint32_t k1, uint64_t q, const LogEntry* lt, float z[8])
+__device__ __forceinline__ void unit_normals<8>(uint32_t k0, uint32_t k1, uint64_t q, const BmTables* tb, float z[8])
 {
-    normals8(k0, k1, q, lt, z);
+    normals8(k0, k1, q, tb, z);
 }
 
 // 16-byte vector loads / stores of one unit.  NT marks the accesses
@@ -237,12 +237,12 @@ template <typename T, int AUX, int ADDR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
 {
     constexpr int N = UnitOf<T>::n;
-    const LogEntry* lt = stage_log_table();
+    const BmTables* tb = stage_bm_tables<kBlock>();
     T* w = static_cast<T*>(a.w);
     auto scalar_body = [&](int64_t u) {
         const int64_t j0 = u * N;
         float z[N];
-        unit_normals<N>(a.k0, a.k1, (uint64_t)(a.noise0 + j0) >> 2, lt, z);
+        unit_normals<N>(a.k0, a.k1, (uint64_t)(a.noise0 + j0) >> 2, tb, z);
 #pragma unroll
         for (int e = 0; e < N; ++e) {
             const int64_t j = j0 + e;
@@ -295,7 +295,7 @@ __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
             if (AUX == kAuxSnapshot) store_vec<T>(static_cast<T*>(a.aux) + j0, old);
         }
         float z[N];
-        unit_normals<N>(a.k0, a.k1, (uint64_t)(a.noise0 + j0) >> 2, lt, z);
+        unit_normals<N>(a.k0, a.k1, (uint64_t)(a.noise0 + j0) >> 2, tb, z);
         T out[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src[e]));
@@ -470,7 +470,7 @@ template <typename T, bool MASTER, int ADDR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
 {
     constexpr int N = MASTER ? 8 : UnitOf<T>::n;
-    const LogEntry* lt = stage_log_table();
+    const BmTables* tb = stage_bm_tables<kBlock>();
     __shared__ float coef[kMaxMembers];
     // Fold members into stream coefficients, in member order, in fp64.
     for (int u = threadIdx.x; u < a.n_streams; u += blockDim.x) {
@@ -488,7 +488,7 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
         for (int s = 0; s < a.n_streams; ++s) {
             const float c = coef[s];
             float z[N];
-            unit_normals<N>(a.seed_lo[s], a.seed_hi[s], (uint64_t)(a.noise0 + j0) >> 2, lt, z);
+            unit_normals<N>(a.seed_lo[s], a.seed_hi[s], (uint64_t)(a.noise0 + j0) >> 2, tb, z);
 #pragma unroll
             for (int e = 0; e < N; ++e) acc[e] = __builtin_fmaf(c, z[e], acc[e]);
         }
@@ -563,7 +563,7 @@ template <typename T, int ADDR>
 __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
 {
     constexpr int N = UnitOf<T>::n;
-    const LogEntry* lt = stage_log_table();
+    const BmTables* tb = stage_bm_tables<kBlock>();
     __shared__ float coef[kMaxMembers];
     for (int u = threadIdx.x; u < a.n_streams; u += blockDim.x) {
         double c = 0.0;
@@ -598,7 +598,7 @@ __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
         for (int st = st0; st < st1; ++st) {
             const float c = coef[st];
             float z[N];
-            unit_normals<N>(a.seed_lo[st], a.seed_hi[st], (uint64_t)j0 >> 2, lt, z);
+            unit_normals<N>(a.seed_lo[st], a.seed_hi[st], (uint64_t)j0 >> 2, tb, z);
 #pragma unroll
             for (int e = 0; e < N; ++e) acc[e] = __builtin_fmaf(c, z[e], acc[e]);
         }
@@ -906,12 +906,12 @@ __global__ __launch_bounds__(kBlock) void k_debug_philox(uint64_t seed, uint32_t
 
 __global__ __launch_bounds__(kBlock) void k_debug_normals(uint64_t seed, int64_t j0, int64_t n, float* out)
 {
-    const LogEntry* lt = stage_log_table();
+    const BmTables* tb = stage_bm_tables<kBlock>();
     const int64_t qa = j0 >> 2;                      // first block touched
     const int64_t qb = (j0 + n + 3) >> 2;            // one past the last
     for (int64_t q = qa + global_tid(); q < qb; q += grid_stride()) {
         float z[4];
-        normals4((uint32_t)seed, (uint32_t)(seed >> 32), (uint64_t)q, lt, z);
+        normals4((uint32_t)seed, (uint32_t)(seed >> 32), (uint64_t)q, tb, z);
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             const int64_t j = 4 * q + t;
@@ -926,15 +926,15 @@ template <typename T, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_fill_normal(T* w, int64_t n, uint64_t seed, uint32_t domain, float stddev)
 {
     constexpr int N = UnitOf<T>::n;
-    const LogEntry* lt = stage_log_table();
+    const BmTables* tb = stage_bm_tables<kBlock>();
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
     auto body = [&](int64_t u, bool vec) {
         const int64_t j0 = u * N;
         float z[N];
         if (N == 8)
-            normals8(k0, k1, (uint64_t)j0 >> 2, lt, z, domain);
+            normals8(k0, k1, (uint64_t)j0 >> 2, tb, z, domain);
         else
-            normals4(k0, k1, (uint64_t)j0 >> 2, lt, z, domain);
+            normals4(k0, k1, (uint64_t)j0 >> 2, tb, z, domain);
         T v[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) v[e] = from_f32<T>(stddev * z[e]);
@@ -953,12 +953,12 @@ __global__ __launch_bounds__(kBlock) void k_fill_normal(T* w, int64_t n, uint64_
 
 __global__ __launch_bounds__(kBlock) void k_debug_bm_grid(uint32_t m0, int64_t n, double* rho, double* c, double* s)
 {
-    const LogEntry* lt = stage_log_table();
+    const BmTables* tb = stage_bm_tables<kBlock>();
     for (int64_t k = global_tid(); k < n; k += grid_stride()) {
         const uint32_t word = (m0 + (uint32_t)k - 1u) << 8;
-        if (rho) rho[k] = bm_radius(word, lt);
+        if (rho) rho[k] = bm_radius(word, tb);
         double cc, ss;
-        bm_angle(word, cc, ss);
+        bm_angle(word, tb, cc, ss);
         if (c) c[k] = cc;
         if (s) s[k] = ss;
     }
@@ -982,12 +982,12 @@ __global__ void k_zero_u32(uint32_t* p)
 
 __global__ __launch_bounds__(kBlock) void k_rng_probe(uint64_t seed, int64_t n, uint32_t* sink)
 {
-    const LogEntry* lt = stage_log_table();
+    const BmTables* tb = stage_bm_tables<kBlock>();
     const int64_t units = (n + 7) / 8;
     uint32_t acc = 0;
     for (int64_t u = global_tid(); u < units; u += grid_stride()) {
         float z[8];
-        normals8((uint32_t)seed, (uint32_t)(seed >> 32), (uint64_t)u * 2u, lt, z);
+        normals8((uint32_t)seed, (uint32_t)(seed >> 32), (uint64_t)u * 2u, tb, z);
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc ^= __float_as_uint(z[e]);
     }

@@ -60,11 +60,15 @@ def test_box_muller_halves_exhaustive(orc, T):
     r_ref = orc.bm_radius_many(words)
     c_ref, s_ref = orc.bm_angle_many(words)
     g_rho, g_c, g_s = to_host(rho), to_host(c), to_host(s)
-    for got, ref in ((g_rho, r_ref), (g_c, c_ref), (g_s, s_ref)):
-        zero = ref == 0
-        assert np.all(got[zero] == 0)
-        rel = np.abs(got[~zero] - ref[~zero]) / np.abs(ref[~zero])
-        assert rel.max() < 2.0 ** -40, rel.max()
+    # U = 1 has radius 0; the device returns 2^-200 there, which still gives a
+    # zero normal in fp32.  The angle's zeros are exact.
+    assert np.all(g_rho[r_ref == 0] == 2.0 ** -200)
+    for got, ref in ((g_c, c_ref), (g_s, s_ref)):
+        assert np.all(got[ref == 0] == 0)
+    for name, got, ref in (("rho", g_rho, r_ref), ("cos", g_c, c_ref), ("sin", g_s, s_ref)):
+        nz = ref != 0
+        rel = np.abs(got[nz] - ref[nz]) / np.abs(ref[nz])
+        assert rel.max() < 2.0 ** -45, (name, np.log2(rel.max()))
 
 
 @pytest.mark.parametrize("seed,j0,n", [
