@@ -1003,7 +1003,7 @@ int64_t grid_for(int64_t work_items, int64_t cap = kMaxGrid)
 }
 
 // Noise kernels on contiguous or chunked subspaces loop over the subspace from
-// a few workgroups per CU (the log table is staged once per workgroup).  On
+// a few workgroups per CU (the tables are staged once per workgroup).  On
 // index maps one workgroup per 256 units is faster: workgroups then start in
 // position order, so the scattered accesses in flight stay in a narrow window
 // of the weights (DRAM row and cache locality).

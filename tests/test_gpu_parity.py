@@ -60,9 +60,11 @@ def test_box_muller_halves_exhaustive(orc, T):
     r_ref = orc.bm_radius_many(words)
     c_ref, s_ref = orc.bm_angle_many(words)
     g_rho, g_c, g_s = to_host(rho), to_host(c), to_host(s)
-    # U = 1 has radius 0; the device returns 2^-200 there, which still gives a
-    # zero normal in fp32.  The angle's zeros are exact.
-    assert np.all(g_rho[r_ref == 0] == 2.0 ** -200)
+    # U = 1 has radius 0; the device returns about 2^-200 there (the square
+    # root of the log table's 2^-400), which still gives a zero normal in fp32.
+    # The angle's zeros are exact.
+    at_one = g_rho[r_ref == 0]
+    assert at_one.size == 1 and 0 < at_one[0] < 2.0 ** -150
     for got, ref in ((g_c, c_ref), (g_s, s_ref)):
         assert np.all(got[ref == 0] == 0)
     for name, got, ref in (("rho", g_rho, r_ref), ("cos", g_c, c_ref), ("sin", g_s, s_ref)):
