@@ -58,7 +58,8 @@ def parse():
                    help="skip the HIP-graph timing (by default one step is also captured in a graph and K replays "
                         "of it are timed: graph_ms_per_step)")
     p.add_argument("--kernels-once", action="store_true",
-                   help="run each kernel once on one 504,654,080-position subspace (for counter passes) and exit")
+                   help="run each kernel once on one subspace (for counter passes) and exit: c3's 504,654,080-position "
+                        "subspace 4, or subspace 0 of a partitioned workload (c4, c4u, c4c)")
     p.add_argument("--cpu-positions", type=int, default=None,
                    help="positions per subspace sample for the oracle baseline (default: 2^31 / members, "
                         "about 10-30 s of host work)")
@@ -365,6 +366,34 @@ def kernels_once(cp, torch):
     print(json.dumps({"kernels_once": "c3 subspace 4", "positions": L}), flush=True)
 
 
+def kernels_once_mapped(W, cp, torch):
+    """The same for a partitioned workload (c4, c4u, c4c): partition once, then
+    one warm-up and one measured launch of each kernel of subspace 0 (perturb
+    taking the backup, perturb from the backup or in place, restore, update),
+    plus torch's copy of the subspace's bf16 bytes as the plain-copy reference."""
+    import synthetic as S
+
+    P = build_plan(W, cp, torch)
+    parts = random_partition(W, cp, P)
+    off, L = parts[0]
+    s = cp.subspace(off, L, P["index"], W.chunk)
+    sigma = float(__import__("numpy").float32(W.sigma * (W.d / L) ** 0.5))
+    snap = P["aux"][:L]
+    later = cp.AUX_BACKUP if W.partition_mode == S.PART_PERMUTATION else cp.AUX_NONE
+    rn = P["rnorm"][0]
+    dst = torch.empty(L, dtype=torch.bfloat16, device="cuda")
+    for _ in range(2):
+        cp.cpes_perturb(P["w"], s, sigma, 3, 1, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+        cp.cpes_restore(P["w"], s, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+        cp.cpes_perturb(P["w"], s, sigma, 4, -1, aux=snap if later == cp.AUX_BACKUP else None, aux_mode=later)
+        cp.cpes_restore(P["w"], s, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+        cp.cpes_normalize_rewards(P["rewards"][0], rn, cp.NORM_Z)
+        cp.cpes_update(P["w"], s, W.member_seeds(0), W.signs, rn, W.alpha, sigma)
+        dst.copy_(P["w"][:L])
+    torch.cuda.synchronize()
+    print(json.dumps({"kernels_once": f"{W.name} subspace 0", "positions": L}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -380,7 +409,10 @@ def main():
     cp.load()
     torch.cuda.set_device(0)
     if args.kernels_once:
-        kernels_once(cp, torch)
+        if W.partition_mode == S.PART_CONTIGUOUS:
+            kernels_once(cp, torch)
+        else:
+            kernels_once_mapped(W, cp, torch)
         return
     P = build_plan(W, cp, torch)
     torch.cuda.synchronize()
