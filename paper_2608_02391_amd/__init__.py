@@ -127,6 +127,26 @@ def _dev_ptr(t, what: str) -> Optional[int]:
     return t.data_ptr()
 
 
+def _need(t, what: str, numel: int, dtype=None) -> None:
+    """A device buffer the kernels will address: it must hold ``numel``
+    elements (of ``dtype`` when given).  The C ABI takes bare pointers and
+    cannot see sizes, so the binding checks them before any launch."""
+    if t is None:
+        return
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{what} must have dtype {dtype}, not {t.dtype}")
+    if t.numel() < numel:
+        raise ValueError(f"{what} holds {t.numel()} elements, {numel} needed")
+
+
+def _aux_need(w, s: "Subspace", aux, aux_mode: int, what: str = "aux") -> None:
+    torch = _torch()
+    if aux_mode == AUX_MASTER:
+        _need(aux, what, s.length, torch.float32)
+    elif aux_mode in (AUX_SNAPSHOT, AUX_BACKUP):
+        _need(aux, what, s.length, w.dtype)
+
+
 def _host_ptr(t, w, s: "Subspace", what: str) -> int:
     """A host backup: a CPU tensor of w's dtype holding at least s.length
     elements.  Whether it is pinned is checked by the library."""
@@ -151,13 +171,17 @@ def _stream(stream) -> Optional[int]:
 
 def subspace(offset: int, length: int, index=None, chunk: int = 0, noise_offset: int = 0) -> Subspace:
     """Positions j < length at parameter offset + j, index[offset + j], or
-    (chunk > 0) index[offset + j // chunk] * chunk + j % chunk.  An int64 map
+    (chunk > 0) index[offset + j // chunk] * chunk + j % chunk; the map must
+    hold the entries those positions read.  An int64 map
     goes to ``index``; a 32-bit map (torch.int32 or torch.uint32 holding the
     uint32 entries of cpes_partition32) goes to ``index32``.  Position j uses
     noise index noise_offset + j (a shard of a larger subspace)."""
     torch = _torch()
     idx64 = idx32 = None
     if index is not None:
+        if length > 0:
+            entries = offset + (-(-length // chunk) if chunk else length)
+            _need(index, "index map", entries)
         if index.dtype == torch.int64:
             idx64 = _dev_ptr(index, "index map")
         elif index.dtype in (torch.int32, getattr(torch, "uint32", torch.int32)):
@@ -177,6 +201,11 @@ def cpes_partition(mode: int, d: int, K: int, seed: int = 0, bounds: Optional[Se
     L = load()
     offsets = (ctypes.c_int64 * (K + 1))()
     b = None if bounds is None else (ctypes.c_int64 * (K + 1))(*[int(x) for x in bounds])
+    if bounds is not None and len(bounds) != K + 1:
+        raise ValueError(f"bounds needs K + 1 = {K + 1} entries, not {len(bounds)}")
+    if mode == PART_PERMUTATION:
+        _need(index, "index", d, _torch().int64)
+    _need(status, "status", 1, _torch().int32)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(L.cpes_partition(mode, d, K, seed, b, offsets, _dev_ptr(index, "index"),
                             _dev_ptr(workspace, "workspace"), ws_bytes, _dev_ptr(status, "status"),
@@ -190,6 +219,8 @@ def cpes_partition32(d: int, K: int, seed: int, index, workspace, status=None, s
     offsets = (ctypes.c_int64 * (K + 1))()
     if index.element_size() != 4:
         raise TypeError("cpes_partition32 writes a 32-bit map")
+    _need(index, "index", d)
+    _need(status, "status", 1, _torch().int32)
     ws_bytes = workspace.numel() * workspace.element_size()
     _check(L.cpes_partition32(d, K, seed, offsets, _dev_ptr(index, "index"), _dev_ptr(workspace, "workspace"),
                               ws_bytes, _dev_ptr(status, "status"), _stream(stream)))
@@ -205,6 +236,8 @@ def cpes_partition_chunks(d: int, chunk: int, K: int, seed: int, chunks, workspa
     L = load()
     offs = (ctypes.c_int64 * (K + 1))()
     lens = (ctypes.c_int64 * K)()
+    _need(chunks, "chunks", -(-d // chunk) if chunk > 0 else 0, _torch().int64)
+    _need(status, "status", 1, _torch().int32)
     ws_bytes = workspace.numel() * workspace.element_size()
     _check(L.cpes_partition_chunks(d, chunk, K, seed, offs, lens, _dev_ptr(chunks, "chunks"),
                                    _dev_ptr(workspace, "workspace"), ws_bytes, _dev_ptr(status, "status"),
@@ -218,12 +251,14 @@ def cpes_partition_chunks_workspace_bytes(d: int, chunk: int, K: int) -> int:
 
 def cpes_perturb(w, s: Subspace, sigma: float, seed: int, sign: int, aux=None, aux_mode: int = AUX_NONE,
                  stream=None) -> None:
+    _aux_need(w, s, aux, aux_mode)
     _check(load().cpes_perturb(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s), sigma, seed, sign,
                                _dev_ptr(aux, "aux"), aux_mode, _stream(stream)))
 
 
 def cpes_restore(w, s: Subspace, sigma: float = 0.0, seed: int = 0, sign: int = 1, aux=None,
                  aux_mode: int = AUX_SNAPSHOT, stream=None) -> None:
+    _aux_need(w, s, aux, aux_mode)
     _check(load().cpes_restore(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s), sigma, seed, sign,
                                _dev_ptr(aux, "aux"), aux_mode, _stream(stream)))
 
@@ -247,12 +282,18 @@ def cpes_fill_normal(w, seed: int, domain: int = 1, stddev: float = 0.02, stream
 
 
 def cpes_stage_master(w, s: Subspace, master, stream=None) -> None:
+    _need(master, "master", s.length, _torch().float32)
     _check(load().cpes_stage_master(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s),
                                     _dev_ptr(master, "master"), _stream(stream)))
 
 
 def cpes_normalize_rewards(r, out, mode: int = NORM_Z, group=None, n_groups: int = 1, status=None,
                            stream=None) -> None:
+    torch = _torch()
+    _need(r, "rewards", 0, torch.float32)
+    _need(out, "out", r.numel(), torch.float32)
+    _need(group, "group", r.numel(), torch.int32)
+    _need(status, "status", 1, torch.int32)
     _check(load().cpes_normalize_rewards(_dev_ptr(r, "rewards"), r.numel(), mode, _dev_ptr(group, "group"),
                                          n_groups, _dev_ptr(out, "out"), _dev_ptr(status, "status"),
                                          _stream(stream)))
@@ -263,6 +304,8 @@ def cpes_update(w, s: Subspace, seeds: Sequence[int], signs: Sequence[int], rnor
     n = len(seeds)
     if len(signs) != n:
         raise ValueError("seeds and signs differ in length")
+    _need(rnorm, "rnorm", n, _torch().float32)
+    _need(master, "master", s.length, _torch().float32)
     cs = (ctypes.c_uint64 * n)(*[int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds])
     cg = (ctypes.c_int8 * n)(*[int(x) for x in signs])
     _check(load().cpes_update(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s),
@@ -286,6 +329,10 @@ def cpes_update_step(w, offsets: Sequence[int], seeds: Sequence[int], signs: Seq
     csg = (ctypes.c_float * K)(*[float(x) for x in sigmas])
     if index is not None and index.dtype != _torch().int64:
         raise TypeError("index map must be int64")
+    if lengths is not None and len(lengths) != K:
+        raise ValueError(f"lengths needs K = {K} entries, not {len(lengths)}")
+    _need(index, "index map", int(offsets[-1]))
+    _need(rnorm, "rnorm", n, _torch().float32)
     cl = None if lengths is None else (ctypes.c_int64 * K)(*[int(x) for x in lengths])
     _check(load().cpes_update_step(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), K, co, _dev_ptr(index, "index"),
                                    int(chunk), cl, n, cs, cg, ck, _dev_ptr(rnorm, "rnorm"), alpha, csg, scale_mode,
@@ -293,24 +340,33 @@ def cpes_update_step(w, offsets: Sequence[int], seeds: Sequence[int], signs: Seq
 
 
 def cpes_debug_philox(seed: int, domain: int, q0: int, nblocks: int, out, stream=None) -> None:
+    if out is not None and out.numel() * out.element_size() < 16 * nblocks:
+        raise ValueError(f"out holds {out.numel() * out.element_size()} bytes, {16 * nblocks} needed")
     _check(load().cpes_debug_philox(seed, domain, q0, nblocks, _dev_ptr(out, "out"), _stream(stream)))
 
 
 def cpes_debug_normals(seed: int, j0: int, n: int, out, stream=None) -> None:
+    _need(out, "out", n, _torch().float32)
     _check(load().cpes_debug_normals(seed, j0, n, _dev_ptr(out, "out"), _stream(stream)))
 
 
 def cpes_debug_bm_grid(m0: int, n: int, rho=None, cos=None, sin=None, stream=None) -> None:
+    for t, what in ((rho, "rho"), (cos, "cos"), (sin, "sin")):
+        _need(t, what, n, _torch().float64)
     _check(load().cpes_debug_bm_grid(m0, n, _dev_ptr(rho, "rho"), _dev_ptr(cos, "cos"), _dev_ptr(sin, "sin"),
                                      _stream(stream)))
 
 
 def cpes_debug_prp(seed: int, d: int, K: int, i0: int, n: int, perm=None, bucket=None, stream=None) -> None:
+    _need(perm, "perm", n, _torch().int64)
+    _need(bucket, "bucket", n, _torch().int32)
     _check(load().cpes_debug_prp(seed, d, K, i0, n, _dev_ptr(perm, "perm"), _dev_ptr(bucket, "bucket"),
                                  _stream(stream)))
 
 
 def cpes_rng_probe(seed: int, n: int, sink, stream=None) -> None:
+    if sink is not None and sink.numel() * sink.element_size() < 4:
+        raise ValueError("sink needs at least 4 bytes")
     _check(load().cpes_rng_probe(seed, n, _dev_ptr(sink, "sink"), _stream(stream)))
 
 

@@ -250,3 +250,37 @@ def test_chunked_subspaces_are_validated(lib):
     assert need > 0 and lib.cpes_partition_chunks_workspace_bytes(1 << 20, 48, 3) == 0
     assert lib.cpes_partition_chunks(1 << 20, 64, 3, 0, offs, lens, FAKE, FAKE, need - 1, None, None) == \
         cp.ERR_WORKSPACE
+
+
+def test_binding_checks_buffer_sizes_and_dtypes(lib):
+    """The C ABI cannot see buffer sizes; the binding rejects undersized or
+    mistyped tensors before any launch (CPU tensors suffice: the checks come
+    before the device-pointer checks)."""
+    torch = pytest.importorskip("torch")
+    w = torch.zeros(64, dtype=torch.bfloat16)
+    s = cp.subspace(0, 32)
+    with pytest.raises(ValueError, match="aux holds 31"):
+        cp.cpes_perturb(w, s, 1e-3, 1, 1, aux=torch.zeros(31, dtype=torch.bfloat16), aux_mode=cp.AUX_SNAPSHOT)
+    with pytest.raises(TypeError, match="aux must have dtype torch.float32"):
+        cp.cpes_perturb(w, s, 1e-3, 1, 1, aux=torch.zeros(32, dtype=torch.bfloat16), aux_mode=cp.AUX_MASTER)
+    with pytest.raises(ValueError, match="aux holds 16"):
+        cp.cpes_restore(w, s, aux=torch.zeros(16, dtype=torch.bfloat16), aux_mode=cp.AUX_SNAPSHOT)
+    with pytest.raises(ValueError, match="master holds"):
+        cp.cpes_stage_master(w, s, torch.zeros(8, dtype=torch.float32))
+    with pytest.raises(ValueError, match="index map holds 40"):
+        cp.subspace(10, 31, torch.zeros(40, dtype=torch.int64))
+    with pytest.raises(ValueError, match="index map holds 3"):              # chunks: offset 1 + ceil(40 / 16)
+        cp.subspace(1, 40, torch.zeros(3, dtype=torch.int64), chunk=16)
+    with pytest.raises(ValueError, match="must be a GPU tensor"):            # size accepted; a host map is not
+        cp.subspace(1, 40, torch.zeros(4, dtype=torch.int64), chunk=16)
+    with pytest.raises(ValueError, match="rnorm holds 3"):
+        cp.cpes_update(w, s, [1, 2, 3, 4], [1, 1, 1, 1], torch.zeros(3, dtype=torch.float32), 5e-4, 1e-3)
+    with pytest.raises(TypeError, match="rnorm must have dtype"):
+        cp.cpes_update(w, s, [1], [1], torch.zeros(1, dtype=torch.float64), 5e-4, 1e-3)
+    with pytest.raises(ValueError, match="out holds 7"):
+        cp.cpes_normalize_rewards(torch.zeros(8), torch.zeros(7), cp.NORM_Z)
+    with pytest.raises(ValueError, match="index holds 99"):
+        cp.cpes_partition(cp.PART_PERMUTATION, 100, 4, 0, index=torch.zeros(99, dtype=torch.int64),
+                          workspace=torch.zeros(16, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="bounds needs K"):
+        cp.cpes_partition(cp.PART_CONTIGUOUS, 100, 4, bounds=[0, 50, 100])
