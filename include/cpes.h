@@ -336,7 +336,9 @@ CPES_API int cpes_debug_normals(uint64_t seed, int64_t j0, int64_t n, float* out
 
 /* The two halves of the normal transform on the grid m = m0 + k, k < n,
  * 1 <= m <= 2^24 (word (m - 1) << 8): rho_dev[k] = sqrt(-2 ln(m 2^-24)),
- * (cos_dev[k], sin_dev[k]) = (cos, sin)(pi m 2^-23), all fp64 (any may be NULL). */
+ * (cos_dev[k], sin_dev[k]) = (cos, sin)(pi m 2^-23), all fp64 (any may be
+ * NULL), as the kernels evaluate them.  At m = 2^24 the radius comes out as
+ * about 2^-200 instead of 0, which still gives a zero normal in fp32. */
 CPES_API int cpes_debug_bm_grid(uint32_t m0, int64_t n, double* rho_dev, double* cos_dev,
                        double* sin_dev, void* stream);
 
