@@ -40,7 +40,6 @@ MEASURED = {
     "update": {"valu_per_normal": 31.3, "hbm_bytes": 4.0},
     "update_master": {"valu_per_normal": 31.2, "hbm_bytes": 10.0},
     "restore": {"hbm_bytes": 4.0},
-    "restore_master": {"hbm_bytes": 6.0},
 }
 
 
@@ -130,7 +129,9 @@ def build_plan(W, cp, torch):
     rewards = torch.from_numpy(np.stack([W.rewards(t) for t in range(n_iter)])).to(dev)
     rnorm = torch.empty_like(rewards)
     host = torch.empty(maxk, dtype=tdt, pin_memory=True) if W.host_backup else None
-    return dict(w=w, index=index, ws=ws, aux=aux, rewards=rewards, rnorm=rnorm, host=host)
+    # master workloads restore from a copy of the weights taken at staging
+    backup = torch.empty(maxk, dtype=tdt, device=dev) if W.master else None
+    return dict(w=w, index=index, ws=ws, aux=aux, rewards=rewards, rnorm=rnorm, host=host, backup=backup)
 
 
 def random_partition(W, cp, P):
@@ -177,8 +178,13 @@ def run_step(W, cp, torch, P, timer, cache, fused=False):
                 timer.run("perturb", lambda: cp.cpes_perturb(P["w"], s, sigmas[k], seed, sign), n_k)
                 timer.run("restore_host", lambda: cp.cpes_restore_from_host(P["w"], s, host), n_k)
             return
+        restore_aux, restore_mode = aux, aux_mode
         if W.master:
             timer.run("stage_master", lambda: cp.cpes_stage_master(P["w"], s, aux), n_k)
+            # w is the master rounded to bf16 now, so a bf16 copy of w restores the
+            # same bits as the master does, reading 2 bytes per position instead of 4
+            restore_aux, restore_mode = P["backup"][:n_k], cp.AUX_SNAPSHOT
+            timer.run("backup", lambda: cp.cpes_backup(P["w"], s, restore_aux), n_k)
         for m, (seed, sign) in enumerate(zip(seeds, signs)):
             # the first member takes the backup of the subspace; the others perturb the
             # restored weights in place, or, on an index map, read the (contiguous)
@@ -190,7 +196,7 @@ def run_step(W, cp, torch, P, timer, cache, fused=False):
                       n_k)
             # (the perturbed model would be evaluated here)
             if not fused or m == len(seeds) - 1:
-                timer.run("restore", lambda: cp.cpes_restore(P["w"], s, aux=aux, aux_mode=aux_mode), n_k)
+                timer.run("restore", lambda: cp.cpes_restore(P["w"], s, aux=restore_aux, aux_mode=restore_mode), n_k)
 
     if W.copes_step:
         # Alg. 1: every subspace gets N/K members, joint standardisation, one composed update
@@ -234,7 +240,9 @@ def bytes_per_position(W, op):
         # write w: the same bytes, one map read)
         return (4 + e if W.master else (3 * e + (m - 1) * 2 * e) / m) + ix
     if op == "restore":
-        return (4 + e if W.master else 2 * e) + ix
+        return 2 * e + ix                              # a bit copy from the backup (taken at staging for a master)
+    if op == "backup":
+        return 2 * e + ix
     if op == "update":
         return (4 + 4 + e if W.master else 2 * e) + ix
     if op == "stage_master":
@@ -309,13 +317,15 @@ def cpu_baseline(W, positions):
         if W.copes_step:
             rn = rn[[i for i, kk in enumerate(W.member_subspaces()) if kk == k]]
         t0 = time.perf_counter()
+        raux, rmode = aux, mode
         if W.master:
             aux[:] = O.stage_master(w, 0, n)
+            raux, rmode = w.copy(), O.AUX_SNAPSHOT          # the GPU schedule: restore from a copy of w
         for m, (seed, sign) in enumerate(zip(seeds, signs)):
             pmode = mode if (W.master or m == 0) else (O.AUX_BACKUP if W.partition_mode == S.PART_PERMUTATION
                                                        else O.AUX_NONE)
             O.perturb(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=pmode)
-            O.restore(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=aux, aux_mode=mode)
+            O.restore(w, 0, n, np.float32(W.sigma_k(k)), seed, sign, aux=raux, aux_mode=rmode)
         O.normalize(W.rewards(0 if W.copes_step else t), W.norm_mode)
         O.update(w, 0, n, seeds, signs, rn, np.float32(W.alpha), np.float32(W.sigma_k(k)), W.scale_mode,
                  master=aux if W.master else None)
@@ -444,7 +454,7 @@ def main():
     span = sum(sizes[k] for k in W.active)                # subspace positions visited per step
     per_sub_members = W.n // W.K if W.copes_step else W.n
     ops = {}
-    for op in ("perturb", "restore", "update", "normalize", "stage_master", "backup_host", "restore_host"):
+    for op in ("perturb", "restore", "update", "normalize", "stage_master", "backup", "backup_host", "restore_host"):
         avg_ms, count, tot_ms = timer.stats(op)
         if count == 0:
             continue
@@ -476,7 +486,7 @@ def main():
                    key=lambda o: ops[o]["ms_per_step"])
     d_entry = ops[dominant]
     gather = W.partition_mode != S.PART_CONTIGUOUS
-    key = dominant + ("_master" if W.master and dominant in ("perturb", "update", "restore") else "")
+    key = dominant + ("_master" if W.master and dominant in ("perturb", "update") else "")
     meas = None if (gather or W.dtype != S.BF16 or W.host_backup) else MEASURED.get(key)
     traffic = None
     if meas is not None:
@@ -484,7 +494,7 @@ def main():
         if per_pos is None:                          # first member takes the backup, the rest read it
             per_pos = (meas["hbm_bytes_first"] + (W.n - 1) * meas["hbm_bytes_rest"]) / W.n
         traffic = round(per_pos * d_entry["positions_per_launch"])
-    if dominant in ("restore", "stage_master"):
+    if dominant in ("restore", "stage_master", "backup"):
         roof = {"bound": "hbm", "achieved": d_entry["GB/s"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(d_entry["GB/s"] / HBM_PEAK_GBPS, 4), "traffic": traffic, "kernel": dominant}
     else:

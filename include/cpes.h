@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define CPES_ABI_VERSION 4
+#define CPES_ABI_VERSION 5
 
 /* Exported symbols (the library is built with hidden default visibility). */
 #define CPES_API __attribute__((visibility("default")))
@@ -234,6 +234,19 @@ CPES_API int cpes_backup_to_host(const void* w_dev, int64_t numel, int dtype, co
                         void* backup_host, void* stream);
 CPES_API int cpes_restore_from_host(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s,
                            const void* backup_host, void* stream);
+
+/*
+ * cpes_backup -- backup_dev[j] = w[p(j)] (bit copy), the weight backup of
+ * Sec. 3.3 taken on its own, in device memory: for a subspace whose members
+ * are perturbed from another source (an fp32 master) but restored from a copy
+ * of the weights.  (A member's perturbation can also take the backup itself:
+ * cpes_perturb with CPES_AUX_SNAPSHOT.)
+ *   backup_dev: s->length elements of `dtype` in device memory, caller-owned;
+ *               it must not overlap w.
+ * Errors: as cpes_perturb for w and s; backup_dev NULL -> CPES_ERR_INVALID_ARGUMENT.
+ */
+CPES_API int cpes_backup(const void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, void* backup_dev,
+                void* stream);
 
 /*
  * cpes_stage_master -- master_dev[j] = fp32 value of w[p(j)] (exact), the fp32

@@ -25,10 +25,10 @@ MAX_MEMBERS, MAX_REWARDS, MAX_GROUPS, MAX_PERMUTATION_K, MAX_STEP_SUBSPACES = 25
 
 EXPORTED = (
     "cpes_partition", "cpes_partition32", "cpes_partition_workspace_bytes", "cpes_partition_chunks",
-    "cpes_partition_chunks_workspace_bytes", "cpes_perturb", "cpes_restore",
-    "cpes_backup_to_host", "cpes_restore_from_host", "cpes_stage_master", "cpes_normalize_rewards", "cpes_update", "cpes_update_step", "cpes_debug_philox",
-    "cpes_debug_normals", "cpes_debug_bm_grid", "cpes_debug_prp", "cpes_rng_probe", "cpes_fill_normal",
-    "cpes_last_error", "cpes_abi_version",
+    "cpes_partition_chunks_workspace_bytes", "cpes_perturb", "cpes_restore", "cpes_backup",
+    "cpes_backup_to_host", "cpes_restore_from_host", "cpes_stage_master", "cpes_normalize_rewards",
+    "cpes_update", "cpes_update_step", "cpes_debug_philox", "cpes_debug_normals", "cpes_debug_bm_grid",
+    "cpes_debug_prp", "cpes_rng_probe", "cpes_fill_normal", "cpes_last_error", "cpes_abi_version",
 )
 
 
@@ -65,6 +65,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "cpes_partition_chunks_workspace_bytes": [i64, i64, i32],
         "cpes_perturb": [vp, i64, i32, sp, f32, u64, i32, vp, i32, vp],
         "cpes_restore": [vp, i64, i32, sp, f32, u64, i32, vp, i32, vp],
+        "cpes_backup": [vp, i64, i32, sp, vp, vp],
         "cpes_backup_to_host": [vp, i64, i32, sp, vp, vp],
         "cpes_restore_from_host": [vp, i64, i32, sp, vp, vp],
         "cpes_stage_master": [vp, i64, i32, sp, vp, vp],
@@ -261,6 +262,13 @@ def cpes_restore(w, s: Subspace, sigma: float = 0.0, seed: int = 0, sign: int = 
     _aux_need(w, s, aux, aux_mode)
     _check(load().cpes_restore(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s), sigma, seed, sign,
                                _dev_ptr(aux, "aux"), aux_mode, _stream(stream)))
+
+
+def cpes_backup(w, s: Subspace, backup, stream=None) -> None:
+    """backup[j] = w[p(j)] into a device tensor of w's dtype."""
+    _need(backup, "backup", s.length, w.dtype)
+    _check(load().cpes_backup(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s),
+                              _dev_ptr(backup, "backup"), _stream(stream)))
 
 
 def cpes_backup_to_host(w, s: Subspace, backup, stream=None) -> None:

@@ -444,6 +444,19 @@ int cpes_restore_from_host(void* w_dev, int64_t numel, int dtype, const cpes_sub
                             "cpes_restore_from_host");
 }
 
+int cpes_backup(const void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, void* backup_dev, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_backup";
+    int rc = check_subspace(w_dev, numel, dtype, s, fn);
+    if (rc) return rc;
+    if (!backup_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: backup pointer is null", fn);
+    if (s->length == 0) return CPES_OK;
+    const cpes::StreamArgs a = stream_args(const_cast<void*>(w_dev), numel, s, backup_dev, 0, 0.0f);
+    const bool vec = vector_ok(w_dev, dtype, s, backup_dev, false);
+    return hip_status(cpes::launch_backup_copy(dtype, addr_mode(s), vec, a, (hipStream_t)stream), fn);
+}
+
 int cpes_stage_master(const void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float* master_dev,
                       void* stream)
 {

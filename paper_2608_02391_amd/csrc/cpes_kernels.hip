@@ -346,7 +346,7 @@ __global__ __launch_bounds__(kBlock) void k_restore_copy(StreamArgs a)
 }
 
 // Backup copy: backup[j] = w[p(j)] (bit copy), for backups taken apart from a
-// perturbation, e.g. into pinned host memory.
+// perturbation, in device memory or in pinned host memory.
 template <typename T, bool NT, int ADDR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_backup_copy(StreamArgs a)
 {

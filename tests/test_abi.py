@@ -37,7 +37,7 @@ def test_header_declares_the_boundary():
 def test_library_exports_every_declared_symbol(lib):
     for name in _declared():
         assert hasattr(lib, name), name
-    assert lib.cpes_abi_version() == 4
+    assert lib.cpes_abi_version() == 5
 
 
 def _sub(offset=0, length=16, index=None, chunk=0, index32=None, noise_offset=0):
@@ -90,7 +90,7 @@ def test_restore_and_stage_reject_bad_arguments(lib):
 
 def test_host_backup_rejects_bad_arguments(lib):
     s = _sub()
-    for fn in (lib.cpes_backup_to_host, lib.cpes_restore_from_host):
+    for fn in (lib.cpes_backup, lib.cpes_backup_to_host, lib.cpes_restore_from_host):
         name = fn.__name__
         for args in [(None, 64, cp.BF16, ctypes.byref(s), FAKE),       # null weights
                      (FAKE, 64, 7, ctypes.byref(s), FAKE),             # bad dtype

@@ -259,6 +259,64 @@ def test_replay_restore_matches_oracle(orc, T, dtype, layout):
         assert f32_close(got, w)
 
 
+# ------------------------------------------------------------ device backup --
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("length", [1, 7, 4095, (1 << 20) + 5])
+@pytest.mark.parametrize("dtype", [S.BF16, S.F32])
+def test_device_backup_is_the_oracle_snapshot(orc, T, dtype, layout, length):
+    """cpes_backup writes the oracle's snapshot bit for bit and leaves w alone;
+    restoring from it undoes a perturbation exactly."""
+    w, dw, off, index, s = _setup(orc, T, dtype, layout, length, 60 + length)
+    w0 = w.copy()
+    b = T.full((length,), 3, dtype=dw.dtype, device="cuda")
+    cp.cpes_backup(dw, s, b)
+    snap = np.zeros(length, dtype=w.dtype)
+    orc.perturb(w.copy(), off, length, np.float32(0.0), 1, 1, index=index, aux=snap, aux_mode=orc.AUX_SNAPSHOT)
+    _sync(T)
+    assert np.array_equal(to_host(b), snap)
+    assert np.array_equal(to_host(dw), w0)
+    cp.cpes_perturb(dw, s, 3e-3, 8, 1)
+    cp.cpes_restore(dw, s, aux=b, aux_mode=cp.AUX_SNAPSHOT)
+    _sync(T)
+    assert np.array_equal(to_host(dw), w0)
+
+
+@pytest.mark.parametrize("layout", ["aligned", "gather", "chunked"])
+def test_master_loop_restores_from_a_bf16_backup(orc, T, layout):
+    """With an fp32 master staged from w, restoring each member from a bf16
+    backup of w gives the same bits as restoring from the master (w is the
+    master rounded to bf16 when both are taken), also after an update."""
+    length = 200003
+    w, dw, off, index, s = _setup(orc, T, S.BF16, layout, length, 91)
+    dw2 = dw.clone()
+    master = T.empty(length, dtype=T.float32, device="cuda")
+    master2 = T.empty_like(master)
+    b = T.empty(length, dtype=T.bfloat16, device="cuda")
+    members = [(21, 1), (21, -1), (22, 1), (22, -1)]
+    rn = to_dev(np.array([0.5, -1.0, 1.5, -1.0], np.float32))
+    for it in range(2):
+        cp.cpes_stage_master(dw, s, master)
+        cp.cpes_stage_master(dw2, s, master2)
+        cp.cpes_backup(dw2, s, b)
+        for seed, sign in members:
+            cp.cpes_perturb(dw, s, 2e-3, seed + it, sign, aux=master, aux_mode=cp.AUX_MASTER)
+            cp.cpes_perturb(dw2, s, 2e-3, seed + it, sign, aux=master2, aux_mode=cp.AUX_MASTER)
+            _sync(T)
+            assert T.equal(dw.view(T.int16), dw2.view(T.int16))
+            cp.cpes_restore(dw, s, aux=master, aux_mode=cp.AUX_MASTER)
+            cp.cpes_restore(dw2, s, aux=b, aux_mode=cp.AUX_SNAPSHOT)
+            _sync(T)
+            assert T.equal(dw.view(T.int16), dw2.view(T.int16))
+        seeds = [m[0] + it for m in members]
+        signs = [m[1] for m in members]
+        cp.cpes_update(dw, s, seeds, signs, rn, 5e-4, 2e-3, master=master)
+        cp.cpes_update(dw2, s, seeds, signs, rn, 5e-4, 2e-3, master=master2)
+        _sync(T)
+        assert T.equal(dw.view(T.int16), dw2.view(T.int16))
+        assert T.equal(master, master2)
+
+
 # ------------------------------------------------------ host-memory backup --
 
 @pytest.mark.parametrize("layout", LAYOUTS)
