@@ -162,9 +162,18 @@ def _host_ptr(t, w, s: "Subspace", what: str) -> int:
     return t.data_ptr()
 
 
+def _current_stream() -> int:
+    """torch's current stream on the current device, as a raw hipStream_t."""
+    torch = _torch()
+    raw, dev = getattr(torch._C, "_cuda_getCurrentRawStream", None), getattr(torch._C, "_cuda_getDevice", None)
+    if raw is not None and dev is not None:
+        return raw(dev())               # the same handle, without building a Stream object per call
+    return torch.cuda.current_stream().cuda_stream
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
-        return _torch().cuda.current_stream().cuda_stream
+        return _current_stream()
     if isinstance(stream, int):
         return stream
     return stream.cuda_stream
