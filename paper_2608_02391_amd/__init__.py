@@ -27,7 +27,7 @@ EXPORTED = (
     "cpes_partition", "cpes_partition32", "cpes_partition_workspace_bytes", "cpes_partition_chunks",
     "cpes_partition_chunks_workspace_bytes", "cpes_perturb", "cpes_restore", "cpes_backup",
     "cpes_backup_to_host", "cpes_restore_from_host", "cpes_stage_master", "cpes_normalize_rewards",
-    "cpes_update", "cpes_update_step", "cpes_debug_philox", "cpes_debug_normals", "cpes_debug_bm_grid",
+    "cpes_update", "cpes_update_step", "cpes_update_step32", "cpes_debug_philox", "cpes_debug_normals", "cpes_debug_bm_grid",
     "cpes_debug_prp", "cpes_rng_probe", "cpes_fill_normal", "cpes_last_error", "cpes_abi_version",
 )
 
@@ -72,6 +72,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "cpes_normalize_rewards": [vp, i32, i32, vp, i32, vp, vp, vp],
         "cpes_update": [vp, i64, i32, sp, vp, i32, vp, vp, vp, f32, f32, i32, vp],
         "cpes_update_step": [vp, i64, i32, i32, vp, vp, i64, vp, i32, vp, vp, vp, vp, f32, vp, i32, vp],
+        "cpes_update_step32": [vp, i64, i32, i32, vp, vp, i32, vp, vp, vp, vp, f32, vp, i32, vp],
         "cpes_debug_philox": [u64, u32, u64, i64, vp, vp],
         "cpes_debug_normals": [u64, i64, i64, vp, vp],
         "cpes_debug_bm_grid": [u32, i64, vp, vp, vp, vp],
@@ -334,7 +335,9 @@ def cpes_update_step(w, offsets: Sequence[int], seeds: Sequence[int], signs: Seq
                      subspaces: Sequence[int], rnorm, alpha: float, sigmas: Sequence[float],
                      scale_mode: int = SCALE_ALPHA_OVER_N_SIGMA, index=None, chunk: int = 0,
                      lengths: Optional[Sequence[int]] = None, stream=None) -> None:
-    """Update every subspace of a partition with its own members (one launch)."""
+    """Update every subspace of a partition with its own members (one launch).
+    ``index``: None (contiguous), an int64 map or chunk list, or a 32-bit map
+    (cpes_partition32) that goes to cpes_update_step32."""
     K = len(offsets) - 1
     n = len(seeds)
     if not (len(signs) == len(subspaces) == n) or len(sigmas) != K:
@@ -344,12 +347,21 @@ def cpes_update_step(w, offsets: Sequence[int], seeds: Sequence[int], signs: Seq
     cg = (ctypes.c_int8 * n)(*[int(x) for x in signs])
     ck = (ctypes.c_int32 * n)(*[int(x) for x in subspaces])
     csg = (ctypes.c_float * K)(*[float(x) for x in sigmas])
-    if index is not None and index.dtype != _torch().int64:
-        raise TypeError("index map must be int64")
+    torch = _torch()
+    idx32 = index is not None and index.dtype in (torch.int32, getattr(torch, "uint32", torch.int32))
+    if index is not None and index.dtype != torch.int64 and not idx32:
+        raise TypeError("index map must be int64, or 32-bit for a uint32 map")
+    if idx32 and chunk:
+        raise ValueError("chunk lists are int64 maps")
     if lengths is not None and len(lengths) != K:
         raise ValueError(f"lengths needs K = {K} entries, not {len(lengths)}")
     _need(index, "index map", int(offsets[-1]))
-    _need(rnorm, "rnorm", n, _torch().float32)
+    _need(rnorm, "rnorm", n, torch.float32)
+    if idx32:
+        _check(load().cpes_update_step32(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), K, co, _dev_ptr(index, "index"),
+                                         n, cs, cg, ck, _dev_ptr(rnorm, "rnorm"), alpha, csg, scale_mode,
+                                         _stream(stream)))
+        return
     cl = None if lengths is None else (ctypes.c_int64 * K)(*[int(x) for x in lengths])
     _check(load().cpes_update_step(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), K, co, _dev_ptr(index, "index"),
                                    int(chunk), cl, n, cs, cg, ck, _dev_ptr(rnorm, "rnorm"), alpha, csg, scale_mode,

@@ -549,14 +549,18 @@ int cpes_update(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, f
     return hip_status(cpes::launch_update(dtype, master_dev != nullptr, addr_mode(s), vec, a, (hipStream_t)stream), fn);
 }
 
-int cpes_update_step(void* w_dev, int64_t numel, int dtype, int32_t K, const int64_t* offsets_host,
-                     const int64_t* index_dev, int64_t chunk, const int64_t* lengths_host, int32_t n,
-                     const uint64_t* seeds_host, const int8_t* signs_host,
-                     const int32_t* subspace_host, const float* rnorm_dev, float alpha, const float* sigma_host,
-                     int scale_mode, void* stream)
+}  // extern "C"
+
+namespace {
+
+// cpes_update_step and cpes_update_step32: the map is int64 entries (or chunk
+// ids), or uint32 entries when idx32.
+int update_step_impl(void* w_dev, int64_t numel, int dtype, int32_t K, const int64_t* offsets_host,
+                     const void* index_dev, bool idx32, int64_t chunk, const int64_t* lengths_host, int32_t n,
+                     const uint64_t* seeds_host, const int8_t* signs_host, const int32_t* subspace_host,
+                     const float* rnorm_dev, float alpha, const float* sigma_host, int scale_mode, void* stream,
+                     const char* fn)
 {
-    g_error.clear();
-    const char* fn = "cpes_update_step";
     if (!w_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: weight pointer is null", fn);
     if (dtype != CPES_BF16 && dtype != CPES_F32) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown dtype %d", fn, dtype);
     if (K < 1) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: K %d < 1", fn, K);
@@ -631,21 +635,53 @@ int cpes_update_step(void* w_dev, int64_t numel, int dtype, int32_t K, const int
         const int64_t units = (len + N - 1) / N;
         if (count[k] > 0) tiles += (units + 63) / 64;   // subspaces without members are left alone
         const void* first = chunk ? w_dev
-                          : index_dev ? (const void*)(index_dev + offsets_host[k])
+                          : index_dev ? (const void*)(static_cast<const char*>(index_dev) +
+                                                      (size_t)offsets_host[k] * (idx32 ? 4 : 8))
                                       : (const void*)(static_cast<const char*>(w_dev) + (size_t)offsets_host[k] * elem_size(dtype));
         if (aligned16(first)) a.vec_mask |= 1u << k;
     }
     a.chunk_shift = chunk ? log2_exact(chunk) : 0;
     a.w = w_dev;
-    a.index = index_dev;
+    a.index = static_cast<const int64_t*>(index_dev);
     a.rnorm = rnorm_dev;
     a.numel = numel;
     a.K = K;
     a.n_members = n;
     a.n_streams = n_streams;
     if (tiles == 0) return CPES_OK;
-    const int addr = !index_dev ? cpes::kAddrContig : chunk ? cpes::kAddrChunk : cpes::kAddrGather;
+    const int addr = !index_dev ? cpes::kAddrContig
+                   : idx32      ? cpes::kAddrGather32
+                   : chunk      ? cpes::kAddrChunk
+                                : cpes::kAddrGather;
     return hip_status(cpes::launch_update_step(dtype, addr, a, (hipStream_t)stream), fn);
+}
+
+}  // namespace
+
+extern "C" {
+
+int cpes_update_step(void* w_dev, int64_t numel, int dtype, int32_t K, const int64_t* offsets_host,
+                     const int64_t* index_dev, int64_t chunk, const int64_t* lengths_host, int32_t n,
+                     const uint64_t* seeds_host, const int8_t* signs_host,
+                     const int32_t* subspace_host, const float* rnorm_dev, float alpha, const float* sigma_host,
+                     int scale_mode, void* stream)
+{
+    g_error.clear();
+    return update_step_impl(w_dev, numel, dtype, K, offsets_host, index_dev, false, chunk, lengths_host, n,
+                            seeds_host, signs_host, subspace_host, rnorm_dev, alpha, sigma_host, scale_mode, stream,
+                            "cpes_update_step");
+}
+
+int cpes_update_step32(void* w_dev, int64_t numel, int dtype, int32_t K, const int64_t* offsets_host,
+                       const uint32_t* index32_dev, int32_t n, const uint64_t* seeds_host, const int8_t* signs_host,
+                       const int32_t* subspace_host, const float* rnorm_dev, float alpha, const float* sigma_host,
+                       int scale_mode, void* stream)
+{
+    g_error.clear();
+    if (!index32_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "cpes_update_step32: index32 map is null");
+    return update_step_impl(w_dev, numel, dtype, K, offsets_host, index32_dev, true, 0, nullptr, n, seeds_host,
+                            signs_host, subspace_host, rnorm_dev, alpha, sigma_host, scale_mode, stream,
+                            "cpes_update_step32");
 }
 
 int cpes_fill_normal(void* w_dev, int64_t n, int dtype, uint64_t seed, uint32_t domain, float stddev, void* stream)

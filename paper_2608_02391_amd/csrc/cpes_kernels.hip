@@ -1107,6 +1107,7 @@ hipError_t update_step_t(int addr, const StepArgs& a, hipStream_t s)
     const int64_t blocks = grid_for(a.tile_begin[a.K] * 64, rng_grid_cap(addr));
     switch (addr) {
     case kGather: hipLaunchKernelGGL((k_update_step<T, kGather>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
+    case kGather32: hipLaunchKernelGGL((k_update_step<T, kGather32>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
     case kChunk: hipLaunchKernelGGL((k_update_step<T, kChunk>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
     default: hipLaunchKernelGGL((k_update_step<T, kContig>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
     }

@@ -64,7 +64,7 @@ constexpr int kMaxStepSubspaces = 32;
 
 struct StepArgs {
     void* w;
-    const int64_t* index;                          // null: contiguous
+    const int64_t* index;                          // null: contiguous (a uint32 map travels in this pointer)
     const float* rnorm;
     int64_t numel;
     int32_t K;

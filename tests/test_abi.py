@@ -234,6 +234,18 @@ def test_update_step_rejects_bad_arguments(lib):
     assert call(index=FAKE, chunk=8, lens=(ctypes.c_int64 * 2)(257, 8)) == cp.ERR_INVALID_ARGUMENT  # > 32 chunks x 8
     assert lib.cpes_last_error().decode().startswith("cpes_update_step")
 
+    def call32(**kw):
+        return lib.cpes_update_step32(kw.get("w", FAKE), kw.get("numel", 64), cp.BF16, kw.get("K", 2),
+                                      kw.get("off", off), kw.get("index", FAKE), 4, seeds, signs,
+                                      kw.get("subs", subs), FAKE, 5e-4, kw.get("sig", sig), 0, None)
+    assert call32(index=None) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_last_error().decode().startswith("cpes_update_step32")
+    assert call32(w=None) == cp.ERR_INVALID_ARGUMENT
+    assert call32(K=40) == cp.ERR_UNSUPPORTED
+    assert call32(subs=bad_subs) == cp.ERR_INVALID_ARGUMENT
+    assert call32(off=dec) == cp.ERR_INVALID_ARGUMENT
+    assert lib.cpes_last_error().decode().startswith("cpes_update_step32")
+
 
 def test_chunked_subspaces_are_validated(lib):
     for chunk, index in ((12, FAKE), (4, FAKE), (1 << 31, FAKE), (64, None)):

@@ -559,6 +559,7 @@ STEP_CASES = {
     # name: (d, K, partition, members per subspace)
     "paper_perm_k4_n40": ((1 << 20) + 3, 4, "perm", [10, 10, 10, 10]),
     "paper_chunk_k4_n40": ((1 << 20) + 3, 4, "chunk", [10, 10, 10, 10]),
+    "paper_perm32_k4_n40": ((1 << 20) + 3, 4, "perm32", [10, 10, 10, 10]),  # uint32 map: cpes_update_step32
     "contig_unaligned": (300007, 3, [0, 1001, 150003, 300007], [5, 3, 4]),
     "contig_k1_std_es": (262147, 1, "equal", [8]),
     "contig_k8_empty": ((1 << 19) + 64, 8, "equal", [2, 0, 3, 1, 1, 0, 2, 2]),
@@ -582,9 +583,9 @@ def test_update_step_matches_oracle(orc, T, case, dtype, scale):
         maps = [orc.expand_chunks(chunks, int(offsets[k]), int(lengths[k]), chunk) for k in range(K)]
         index = np.concatenate(maps)
         host_offsets = np.concatenate([[0], np.cumsum(lengths)])
-    elif part == "perm":
+    elif part in ("perm", "perm32"):
         offsets, index = orc.partition(orc.PART_PERMUTATION, d, K, seed=33)
-        dindex = to_dev(index)
+        dindex = to_dev(index if part == "perm" else index.astype(np.uint32).view(np.int32))
     elif part == "equal":
         offsets, _ = orc.partition(orc.PART_CONTIGUOUS, d, K)
     else:
