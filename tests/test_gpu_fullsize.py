@@ -210,10 +210,13 @@ def test_c5_master_iteration(orc, T, big):
     full_before = w.clone()
     s = cp.subspace(off, L)
     master = T.empty(L, dtype=T.float32, device="cuda")
-    _say("c5: stage master, perturb / restore from master")
+    _say("c5: stage master and bf16 backup, perturb from master, restore from the backup and from master")
     cp.cpes_stage_master(w, s, master)
+    backup = T.empty(L, dtype=T.bfloat16, device="cuda")
+    cp.cpes_backup(w, s, backup)                       # the schedule bench.py times
     T.cuda.synchronize()
     assert T.equal(master, full_before[off:off + L].float())
+    assert T.equal(backup, full_before[off:off + L])
     seeds = W.member_seeds(t)
     for m in (0, 1, 127):
         cp.cpes_perturb(w, s, sigma, seeds[m], W.signs[m], aux=master, aux_mode=cp.AUX_MASTER)
@@ -223,9 +226,13 @@ def test_c5_master_iteration(orc, T, big):
         mref = orc.bf16_to_f32(before[p]).copy()
         orc.perturb(ref, 0, WIN, np.float32(sigma), seeds[m], W.signs[m], j0=p, aux=mref, aux_mode=orc.AUX_MASTER)
         assert ulp_bf16(_host_bits(w[off + p: off + p + WIN]), ref).max() <= 1
-        cp.cpes_restore(w, s, aux=master, aux_mode=cp.AUX_MASTER)
-    T.cuda.synchronize()
-    assert T.equal(w, full_before)
+        if m == 1:
+            cp.cpes_restore(w, s, aux=master, aux_mode=cp.AUX_MASTER)
+        else:
+            cp.cpes_restore(w, s, aux=backup, aux_mode=cp.AUX_SNAPSHOT)
+        T.cuda.synchronize()
+        assert T.equal(w, full_before)
+    del backup
     _say("c5: update of master and bf16 weights with 128 antithetic members")
     r = W.rewards(t)
     rn_ref, _ = orc.normalize(r, W.norm_mode)
