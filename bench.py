@@ -407,8 +407,8 @@ def kernels_once_mapped(W, cp, torch):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU "
-              "path, see DESIGN.md for how it would shard.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the library has no multi-GPU "
+              "path: a population would shard across GPUs by member, with a reward all-gather.", file=sys.stderr)
         sys.exit(2)
     import torch
 

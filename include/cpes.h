@@ -69,7 +69,7 @@ extern "C" {
 enum cpes_status {
     CPES_OK = 0,
     CPES_ERR_INVALID_ARGUMENT = -1, /* a null, out-of-range or inconsistent argument */
-    CPES_ERR_UNSUPPORTED = -2,      /* valid but beyond this build's limits (see each call) */
+    CPES_ERR_UNSUPPORTED = -2,      /* valid but beyond the library's limits (see each call) */
     CPES_ERR_WORKSPACE = -3,        /* workspace missing or smaller than required */
     CPES_ERR_HIP = -4,              /* the HIP runtime reported an error while enqueueing */
 };
@@ -80,7 +80,7 @@ enum cpes_aux_mode { CPES_AUX_NONE = 0, CPES_AUX_SNAPSHOT = 1, CPES_AUX_MASTER =
 enum cpes_norm_mode { CPES_NORM_Z = 0, CPES_NORM_RANK = 1 };
 enum cpes_scale_mode { CPES_SCALE_ALPHA_OVER_N_SIGMA = 0, CPES_SCALE_ALPHA_OVER_N = 1 };
 
-/* Limits of this build. */
+/* Limits of the library. */
 #define CPES_MAX_MEMBERS 256         /* members per cpes_update call */
 #define CPES_MAX_REWARDS 4096        /* rewards per cpes_normalize_rewards call */
 #define CPES_MAX_GROUPS 1024         /* reward groups per cpes_normalize_rewards call */
