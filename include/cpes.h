@@ -149,8 +149,8 @@ CPES_API size_t cpes_partition_workspace_bytes(int mode, int64_t d, int32_t K);
 
 /*
  * cpes_partition_chunks -- the chunk-granular random partition the paper runs
- * (Sec. 3.3; Supp. A.8 "Partition Replay": chunk-to-subspace assignments
- * replayed from a stored seed).  The d parameters form n_chunks = ceil(d /
+ * (Sec. 3.3; Supp. A.8 "Partition Replay": the assignment of chunks to
+ * subspaces is replayed from a stored seed).  The d parameters form n_chunks = ceil(d /
  * chunk) chunks of `chunk` consecutive parameters (the last may be shorter);
  * chunk c belongs to subspace floor(E(c) K / n_chunks), E being the keyed
  * permutation of cpes_partition (CPES_PART_PERMUTATION) on [0, n_chunks).
