@@ -30,6 +30,10 @@ Workloads (weights N(0, 0.02); sigma = 1e-3; alpha = 5e-4 unless stated):
   buffer, K = 4 chunk-granular random subspaces (chunks of 65,536), N = 40
   members split 10 per subspace, rewards U[0,1) standardised jointly (Eq. 12),
   update alpha / N_k (Eq. 13) over all subspaces in one call.
+* ``c3h``, ``p0h`` -- c3 and p0 with the weight backup in pinned host memory
+  (the backup of Sec. 3.3 kept off the GPU).
+* ``c4u`` -- c4 with uint32 index maps (the model has fewer than 2^32
+  parameters).
 
 The effective perturbation scale passed to the library is
 sigma_k = sigma * sqrt(d / d_k) (the dimension-aware scale of Eq. 11).
