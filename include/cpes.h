@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define CPES_ABI_VERSION 5
+#define CPES_ABI_VERSION 6
 
 /* Exported symbols (the library is built with hidden default visibility). */
 #define CPES_API __attribute__((visibility("default")))
@@ -377,6 +377,22 @@ CPES_API int cpes_debug_prp(uint64_t seed, int64_t d, int32_t K, int64_t i0, int
  * 0 .. n-1) and folds them into sink_dev[0] (one uint32, overwritten) without
  * other memory traffic, to measure the generator's ALU ceiling. */
 CPES_API int cpes_rng_probe(uint64_t seed, int64_t n, uint32_t* sink_dev, void* stream);
+
+/* Measurement references for the map and copy kernels: the same memory
+ * traffic with nothing else, timed beside them.
+ * cpes_probe_map_copy: the plainest gather (direction 0: buf[j] = w[p(j)])
+ *   or scatter (direction 1: w[p(j)] = buf[j]) through the element map of
+ *   `s` (index or index32; no chunk lists), one position per thread.  buf_dev:
+ *   s->length elements of `dtype`, device memory.  Entries outside
+ *   [0, numel) are skipped.
+ * cpes_probe_copy: dst[i] = src[i] over `bytes` bytes (a multiple of 16; both
+ *   pointers 16-byte aligned device memory), one 16-byte vector per thread.
+ * Errors: null pointers, a subspace without an element map, direction not 0
+ *   or 1, bytes negative or not a multiple of 16, misaligned pointers ->
+ *   CPES_ERR_INVALID_ARGUMENT. */
+CPES_API int cpes_probe_map_copy(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, void* buf_dev,
+                                 int direction, void* stream);
+CPES_API int cpes_probe_copy(const void* src_dev, void* dst_dev, int64_t bytes, void* stream);
 
 /* Message of the last error on the calling thread ("" if none). */
 CPES_API const char* cpes_last_error(void);

@@ -28,7 +28,8 @@ EXPORTED = (
     "cpes_partition_chunks_workspace_bytes", "cpes_perturb", "cpes_restore", "cpes_backup",
     "cpes_backup_to_host", "cpes_restore_from_host", "cpes_stage_master", "cpes_normalize_rewards",
     "cpes_update", "cpes_update_step", "cpes_update_step32", "cpes_debug_philox", "cpes_debug_normals", "cpes_debug_bm_grid",
-    "cpes_debug_prp", "cpes_rng_probe", "cpes_fill_normal", "cpes_last_error", "cpes_abi_version",
+    "cpes_debug_prp", "cpes_rng_probe", "cpes_probe_map_copy", "cpes_probe_copy", "cpes_fill_normal",
+    "cpes_last_error", "cpes_abi_version",
 )
 
 
@@ -78,6 +79,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "cpes_debug_bm_grid": [u32, i64, vp, vp, vp, vp],
         "cpes_debug_prp": [u64, i64, i32, i64, i64, vp, vp, vp],
         "cpes_rng_probe": [u64, i64, vp, vp],
+        "cpes_probe_map_copy": [vp, i64, i32, sp, vp, i32, vp],
+        "cpes_probe_copy": [vp, vp, i64, vp],
         "cpes_fill_normal": [vp, i64, i32, u64, u32, f32, vp],
         "cpes_last_error": [],
         "cpes_abi_version": [],
@@ -397,6 +400,22 @@ def cpes_rng_probe(seed: int, n: int, sink, stream=None) -> None:
     if sink is not None and sink.numel() * sink.element_size() < 4:
         raise ValueError("sink needs at least 4 bytes")
     _check(load().cpes_rng_probe(seed, n, _dev_ptr(sink, "sink"), _stream(stream)))
+
+
+def cpes_probe_map_copy(w, s: Subspace, buf, direction: int, stream=None) -> None:
+    """Plain gather (direction 0: buf[j] = w[p(j)]) or scatter (1: w[p(j)] =
+    buf[j]) through the subspace's element map: a measurement reference."""
+    _need(buf, "buf", s.length, w.dtype)
+    _check(load().cpes_probe_map_copy(_dev_ptr(w, "w"), w.numel(), _dtype_code(w), ctypes.byref(s),
+                                      _dev_ptr(buf, "buf"), direction, _stream(stream)))
+
+
+def cpes_probe_copy(src, dst, nbytes: int, stream=None) -> None:
+    """dst[:nbytes] = src[:nbytes], one 16-byte vector per thread: a measurement reference."""
+    for t, what in ((src, "src"), (dst, "dst")):
+        if t.numel() * t.element_size() < nbytes:
+            raise ValueError(f"{what} holds fewer than {nbytes} bytes")
+    _check(load().cpes_probe_copy(_dev_ptr(src, "src"), _dev_ptr(dst, "dst"), nbytes, _stream(stream)))
 
 
 def cpes_abi_version() -> int:

@@ -102,14 +102,14 @@ int check_sigma(float sigma, const char* fn)
 }
 
 // Whether the 16-byte vector path applies: every unit's vectors are aligned.
+// Element maps are read one entry per lane, and the weights they address one
+// element at a time, so only the side buffer's alignment matters for them.
 bool vector_ok(const void* w, int dtype, const cpes_subspace* s, const void* aux, bool aux_is_master)
 {
     if (s->index && s->chunk) {
         if (!aligned16(w)) return false;                    // chunk starts are multiples of 8 elements
-    } else if (s->index) {
-        if (!aligned16(s->index + s->offset)) return false;
-    } else if (s->index32) {
-        if (!aligned16(s->index32 + s->offset)) return false;
+    } else if (s->index || s->index32) {
+        // nothing: the map kernels take any map offset
     } else {
         const char* base = static_cast<const char*>(w) + (size_t)s->offset * elem_size(dtype);
         if (!aligned16(base)) return false;
@@ -734,6 +734,36 @@ int cpes_debug_prp(uint64_t seed, int64_t d, int32_t K, int64_t i0, int64_t n, i
     return hip_status(cpes::launch_debug_prp(seed, d, K, feistel_half_bits(d), i0, n, perm_dev, bucket_dev,
                                              (hipStream_t)stream),
                       "cpes_debug_prp");
+}
+
+int cpes_probe_map_copy(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, void* buf_dev, int direction,
+                        void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_probe_map_copy";
+    int rc = check_subspace(w_dev, numel, dtype, s, fn);
+    if (rc) return rc;
+    if ((!s->index && !s->index32) || s->chunk != 0)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: needs an element map (index or index32)", fn);
+    if (!buf_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: buffer is null", fn);
+    if (direction != 0 && direction != 1)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: direction %d is not 0 (gather) or 1 (scatter)", fn, direction);
+    if (s->length == 0) return CPES_OK;
+    const cpes::StreamArgs a = stream_args(w_dev, numel, s, buf_dev, 0, 0.0f);
+    return hip_status(cpes::launch_probe_map_copy(dtype, addr_mode(s), direction, a, (hipStream_t)stream), fn);
+}
+
+int cpes_probe_copy(const void* src_dev, void* dst_dev, int64_t bytes, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_probe_copy";
+    if (!src_dev || !dst_dev) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: null pointer", fn);
+    if (bytes < 0 || (bytes & 15) != 0)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: bytes %lld is negative or not a multiple of 16", fn, (long long)bytes);
+    if (!aligned16(src_dev) || !aligned16(dst_dev))
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: pointers must be 16-byte aligned", fn);
+    if (bytes == 0) return CPES_OK;
+    return hip_status(cpes::launch_probe_copy(src_dev, dst_dev, bytes, (hipStream_t)stream), fn);
 }
 
 int cpes_rng_probe(uint64_t seed, int64_t n, uint32_t* sink_dev, void* stream)

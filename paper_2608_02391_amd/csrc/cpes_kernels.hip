@@ -85,17 +85,6 @@ __device__ __forceinline__ void store_f32s(float* p, const float v[N])
             reinterpret_cast<V4f*>(p)[h] = x;
     }
 }
-template <int N>
-__device__ __forceinline__ void load_index(const int64_t* p, int64_t v[N])
-{
-#pragma unroll
-    for (int h = 0; h < N / 2; ++h) {
-        const longlong2 x = reinterpret_cast<const longlong2*>(p)[h];
-        v[2 * h] = x.x;
-        v[2 * h + 1] = x.y;
-    }
-}
-
 __device__ __forceinline__ int64_t grid_stride() { return (int64_t)gridDim.x * blockDim.x; }
 __device__ __forceinline__ int64_t global_tid() { return (int64_t)blockIdx.x * blockDim.x + threadIdx.x; }
 
@@ -107,44 +96,6 @@ constexpr int kContig = kAddrContig, kGather = kAddrGather, kChunk = kAddrChunk,
 // An element-level map (int64 or uint32 entries).
 template <int ADDR>
 constexpr bool kMap = ADDR == kGather || ADDR == kGather32;
-
-// The map entries of positions p .. p + N - 1 (16-byte loads; p + index must
-// be 16-byte aligned), widened to int64.
-template <int ADDR, int N>
-__device__ __forceinline__ void load_map(const int64_t* index, int64_t p, int64_t v[N])
-{
-    if (ADDR == kGather) {
-        load_index<N>(index + p, v);
-    } else {
-        const uint4* q = reinterpret_cast<const uint4*>(reinterpret_cast<const uint32_t*>(index) + p);
-#pragma unroll
-        for (int h = 0; h < N / 4; ++h) {
-            const uint4 x = q[h];
-            v[4 * h + 0] = x.x; v[4 * h + 1] = x.y; v[4 * h + 2] = x.z; v[4 * h + 3] = x.w;
-        }
-    }
-}
-
-// Scatter one unit through a map.  When every entry is valid (always, for a
-// partition's own map) the stores run without per-element branches, so they
-// issue back to back: with a branch around each store the wait for the loaded
-// data is repeated before every store and, since stores share the vector
-// memory counter, each store then waits for the one before it.
-template <typename T, int N>
-__device__ __forceinline__ void scatter_unit(T* w, const int64_t idx[N], const T v[N], int64_t numel)
-{
-    uint32_t bad = 0;   // bitwise, not short-circuit: keeps the check free of branches
-#pragma unroll
-    for (int e = 0; e < N; ++e) bad |= (uint64_t)idx[e] >= (uint64_t)numel ? 1u : 0u;
-    if (bad == 0) {
-#pragma unroll
-        for (int e = 0; e < N; ++e) w[idx[e]] = v[e];
-    } else {
-#pragma unroll
-        for (int e = 0; e < N; ++e)
-            if (idx[e] >= 0 && idx[e] < numel) w[idx[e]] = v[e];
-    }
-}
 
 // Resolve the parameter index of position j; returns false for a map entry
 // outside [0, numel) (skipped, never dereferenced).
@@ -232,7 +183,8 @@ __device__ __forceinline__ void for_each_unit(int64_t length, VecBody&& vec_body
 // ---------------------------------------------------------------- perturb --
 // w[p(j)] = cast(fmaf(scale, eps_j, src_j)); src = w (optionally backed up to
 // the snapshot first), the fp32 master, or an existing backup.  Also serves
-// replay restore with scale = -sign * sigma.
+// replay restore with scale = -sign * sigma.  Contiguous and chunked
+// subspaces; index maps take k_perturb_map below.
 template <typename T, int AUX, int ADDR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
 {
@@ -264,24 +216,13 @@ __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
     auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
         int64_t base = 0;
-        int64_t idx[N];
-        if (kMap<ADDR>) {
-            load_map<ADDR, N>(a.index, a.offset + j0, idx);
-        } else if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+        if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
             scalar_body(u);
             return;
         }
         float src[N];
         T old[N];
-        if (kMap<ADDR> && AUX != kAuxMaster && AUX != kAuxBackup) {
-#pragma unroll
-            for (int e = 0; e < N; ++e) {
-                const bool ok = idx[e] >= 0 && idx[e] < a.numel;
-                old[e] = ok ? w[idx[e]] : T(0);
-            }
-        } else if (AUX != kAuxMaster && AUX != kAuxBackup) {
-            load_vec<T>(w + base, old);
-        }
+        if (AUX != kAuxMaster && AUX != kAuxBackup) load_vec<T>(w + base, old);
         if (AUX == kAuxMaster) {
             load_f32s<N>(static_cast<const float*>(a.aux) + j0, src);
         } else if (AUX == kAuxBackup) {
@@ -299,11 +240,7 @@ __global__ __launch_bounds__(kBlock) void k_perturb(StreamArgs a)
         T out[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src[e]));
-        if (kMap<ADDR>) {
-            scatter_unit<T, N>(w, idx, out, a.numel);
-        } else {
-            store_vec<T>(w + base, out);
-        }
+        store_vec<T>(w + base, out);
     };
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
@@ -327,20 +264,14 @@ __global__ __launch_bounds__(kBlock) void k_restore_copy(StreamArgs a)
     };
     auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
+        int64_t base;
+        if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+            scalar_body(u);
+            return;
+        }
         T v[N];
         load_vec<T, NT>(snap + j0, v);
-        if (kMap<ADDR>) {
-            int64_t idx[N];
-            load_map<ADDR, N>(a.index, a.offset + j0, idx);
-            scatter_unit<T, N>(w, idx, v, a.numel);
-        } else {
-            int64_t base;
-            if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
-                scalar_body(u);
-                return;
-            }
-            store_vec<T, NT>(w + base, v);
-        }
+        store_vec<T, NT>(w + base, v);
     };
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
@@ -364,20 +295,13 @@ __global__ __launch_bounds__(kBlock) void k_backup_copy(StreamArgs a)
     };
     auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
-        T v[N];
-        if (kMap<ADDR>) {
-            int64_t idx[N];
-            load_map<ADDR, N>(a.index, a.offset + j0, idx);
-#pragma unroll
-            for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
-        } else {
-            int64_t base;
-            if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
-                scalar_body(u);
-                return;
-            }
-            load_vec<T, NT>(w + base, v);
+        int64_t base;
+        if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+            scalar_body(u);
+            return;
         }
+        T v[N];
+        load_vec<T, NT>(w + base, v);
         store_vec<T, NT>(backup + j0, v);
     };
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
@@ -401,23 +325,17 @@ __global__ __launch_bounds__(kBlock) void k_restore_master(StreamArgs a)
     };
     auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
+        int64_t base;
+        if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+            scalar_body(u);
+            return;
+        }
         float m[N];
         load_f32s<N, NT>(master + j0, m);
         uint16_t v[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) v[e] = f32_to_bf16(m[e]);
-        if (kMap<ADDR>) {
-            int64_t idx[N];
-            load_map<ADDR, N>(a.index, a.offset + j0, idx);
-            scatter_unit<uint16_t, N>(w, idx, v, a.numel);
-        } else {
-            int64_t base;
-            if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
-                scalar_body(u);
-                return;
-            }
-            store_vec<uint16_t, NT>(w + base, v);
-        }
+        store_vec<uint16_t, NT>(w + base, v);
     };
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
 }
@@ -440,20 +358,13 @@ __global__ __launch_bounds__(kBlock) void k_stage_master(StreamArgs a)
     };
     auto vec_body = [&](int64_t u) {
         const int64_t j0 = u * N;
-        T v[N];
-        if (kMap<ADDR>) {
-            int64_t idx[N];
-            load_map<ADDR, N>(a.index, a.offset + j0, idx);
-#pragma unroll
-            for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
-        } else {
-            int64_t base;
-            if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
-                scalar_body(u);
-                return;
-            }
-            load_vec<T, NT>(w + base, v);
+        int64_t base;
+        if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+            scalar_body(u);
+            return;
         }
+        T v[N];
+        load_vec<T, NT>(w + base, v);
         float m[N];
 #pragma unroll
         for (int e = 0; e < N; ++e) m[e] = to_f32<T>(v[e]);
@@ -466,32 +377,48 @@ __global__ __launch_bounds__(kBlock) void k_stage_master(StreamArgs a)
 // theta_S += step * sum_u c_u eps_u, c_u = sum over members of stream u of
 // sign * rnorm.  Each thread reads its unit of weights once, regenerates every
 // stream's noise for it in registers, accumulates in fp32 and writes once.
+
+// Fold members into stream coefficients, in member order, in fp64.
+__device__ __forceinline__ void fold_coefficients(const int32_t n_members, const int32_t n_streams,
+                                                  const uint8_t* member_stream, const int8_t* member_sign,
+                                                  const float* rnorm, float* coef)
+{
+    for (int u = threadIdx.x; u < n_streams; u += blockDim.x) {
+        double c = 0.0;
+        for (int i = 0; i < n_members; ++i)
+            if (member_stream[i] == u) c += (double)member_sign[i] * (double)rnorm[i];
+        coef[u] = (float)c;
+    }
+    __syncthreads();
+}
+
+// acc[e] = sum over streams s0 <= s < s1 of coef[s] * eps_s(q-th block pair), in stream order.
+template <int N>
+__device__ __forceinline__ void accumulate_streams(const uint32_t* seed_lo, const uint32_t* seed_hi, const float* coef,
+                                                   int s0, int s1, uint64_t q, const BmTables* tb, float acc[N])
+{
+#pragma unroll
+    for (int e = 0; e < N; ++e) acc[e] = 0.0f;
+    for (int s = s0; s < s1; ++s) {
+        const float c = coef[s];
+        float z[N];
+        unit_normals<N>(seed_lo[s], seed_hi[s], q, tb, z);
+#pragma unroll
+        for (int e = 0; e < N; ++e) acc[e] = __builtin_fmaf(c, z[e], acc[e]);
+    }
+}
+
 template <typename T, bool MASTER, int ADDR, bool VEC>
 __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
 {
     constexpr int N = MASTER ? 8 : UnitOf<T>::n;
     const BmTables* tb = stage_bm_tables<kBlock>();
     __shared__ float coef[kMaxMembers];
-    // Fold members into stream coefficients, in member order, in fp64.
-    for (int u = threadIdx.x; u < a.n_streams; u += blockDim.x) {
-        double c = 0.0;
-        for (int i = 0; i < a.n_members; ++i)
-            if (a.member_stream[i] == u) c += (double)a.member_sign[i] * (double)a.rnorm[i];
-        coef[u] = (float)c;
-    }
-    __syncthreads();
+    fold_coefficients(a.n_members, a.n_streams, a.member_stream, a.member_sign, a.rnorm, coef);
 
     T* w = static_cast<T*>(a.w);
     auto accumulate = [&](int64_t j0, float acc[N]) {
-#pragma unroll
-        for (int e = 0; e < N; ++e) acc[e] = 0.0f;
-        for (int s = 0; s < a.n_streams; ++s) {
-            const float c = coef[s];
-            float z[N];
-            unit_normals<N>(a.seed_lo[s], a.seed_hi[s], (uint64_t)(a.noise0 + j0) >> 2, tb, z);
-#pragma unroll
-            for (int e = 0; e < N; ++e) acc[e] = __builtin_fmaf(c, z[e], acc[e]);
-        }
+        accumulate_streams<N>(a.seed_lo, a.seed_hi, coef, 0, a.n_streams, (uint64_t)(a.noise0 + j0) >> 2, tb, acc);
     };
     auto scalar_finish = [&](int64_t j0, const float acc[N]) {
 #pragma unroll
@@ -517,20 +444,13 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
         const int64_t j0 = u * N;
         float acc[N];
         accumulate(j0, acc);
-        int64_t idx[N];
         int64_t base = 0;
         T v[N];
-        if (kMap<ADDR>) {
-            load_map<ADDR, N>(a.index, a.offset + j0, idx);
-#pragma unroll
-            for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
-        } else {
-            if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
-                scalar_finish(j0, acc);
-                return;
-            }
-            if (!MASTER) load_vec<T>(w + base, v);
+        if (!unit_base<ADDR>(a.index, a.offset, a.numel, a.chunk_shift, j0, N, base)) {
+            scalar_finish(j0, acc);
+            return;
         }
+        if (!MASTER) load_vec<T>(w + base, v);
         T out[N];
         if (MASTER) {
             float m[N];
@@ -545,39 +465,317 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdateArgs a)
 #pragma unroll
             for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.step, acc[e], to_f32<T>(v[e])));
         }
-        if (kMap<ADDR>) {
-            scatter_unit<T, N>(w, idx, out, a.numel);
-        } else {
-            store_vec<T>(w + base, out);
-        }
+        store_vec<T>(w + base, out);
     };
     for_each_unit<N, VEC>(a.length, vec_body, scalar_body);
+}
+
+// ------------------------------------------------------- index-map kernels --
+// Subspaces given by an element map (int64 or uint32 entries; a partition's
+// maps are ascending, at density d_k / d across the weights).  A wave owns
+// tiles of 64 N consecutive positions.  Map entries, and the weights they
+// address, are taken lane-interleaved: lane l handles positions t0 + l + 64 e,
+// e < N.  Each memory instruction then covers 64 consecutive map entries, a
+// window of about 64 d / d_k consecutive weights (a few 128-byte lines), where
+// a unit per lane would touch 64 windows that far apart.  Noise comes in
+// units of N consecutive positions per lane, and so do contiguous side
+// buffers (backup, master); a per-wave LDS buffer of one tile converts
+// between the two layouts.
+
+template <int ADDR>
+__device__ __forceinline__ int64_t map_entry(const int64_t* index, int64_t p)
+{
+    if (ADDR == kGather) return index[p];
+    return (int64_t)reinterpret_cast<const uint32_t*>(index)[p];
+}
+
+// The wave's index and the number of waves in the grid (uniform in a wave).
+__device__ __forceinline__ int64_t wave_id()
+{
+    return (int64_t)blockIdx.x * (kBlock / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+}
+__device__ __forceinline__ int64_t wave_count() { return (int64_t)gridDim.x * (kBlock / 64); }
+
+// Parameters of lane `lane`'s positions in the tile at t0:
+// idx[e] = map[offset + t0 + lane + 64 e], or -1 beyond the subspace or for
+// an entry outside [0, numel) (skipped, never dereferenced).  Returns true
+// when every entry of the wave is valid (a full tile of a partition's map).
+template <int ADDR, int N>
+__device__ __forceinline__ bool tile_entries(const int64_t* index, int64_t offset, int64_t length, int64_t numel,
+                                             int64_t t0, int lane, int64_t idx[N])
+{
+    bool ok = true;
+    if (t0 + 64 * N <= length) {
+#pragma unroll
+        for (int e = 0; e < N; ++e) idx[e] = map_entry<ADDR>(index, offset + t0 + lane + 64 * e);
+    } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+            const int64_t j = t0 + lane + 64 * e;
+            idx[e] = j < length ? map_entry<ADDR>(index, offset + j) : -1;
+        }
+        ok = false;
+    }
+#pragma unroll
+    for (int e = 0; e < N; ++e)
+        if ((uint64_t)idx[e] >= (uint64_t)numel) {
+            idx[e] = -1;
+            ok = false;
+        }
+    return __builtin_amdgcn_ballot_w64(!ok) == 0;
+}
+
+// Gather w at the tile's entries (lane-interleaved); skipped entries read 0.
+template <typename T, int N>
+__device__ __forceinline__ void gather_lanes(const T* w, const int64_t idx[N], bool all_valid, T v[N])
+{
+    if (all_valid) {
+#pragma unroll
+        for (int e = 0; e < N; ++e) v[e] = w[idx[e]];
+    } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e) v[e] = idx[e] >= 0 ? w[idx[e]] : T(0);
+    }
+}
+
+// Scatter lane-interleaved values.  With every entry valid the stores carry
+// no branch and issue back to back; a branch around each store would make the
+// compiler wait for the loaded data before every one of them.
+template <typename T, int N>
+__device__ __forceinline__ void scatter_lanes(T* w, const int64_t idx[N], bool all_valid, const T v[N])
+{
+    if (all_valid) {
+#pragma unroll
+        for (int e = 0; e < N; ++e) w[idx[e]] = v[e];
+    } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e)
+            if (idx[e] >= 0) w[idx[e]] = v[e];
+    }
+}
+
+// Lane-level ordering of the exchange buffer: LDS accesses of one wave take
+// effect in program order, so the compiler only has to keep them in order.
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+}
+
+// Units (lane l holds positions N l .. N l + N - 1 of the tile) to lanes
+// (lane l holds l + 64 e), and back, through the wave's tile buffer `buf`
+// (64 N elements, 16-byte aligned).
+template <typename T, int N>
+__device__ __forceinline__ void units_to_lanes(T* buf, int lane, const T in[N], T out[N])
+{
+    static_assert(N * sizeof(T) == 16, "a unit is one 16-byte vector");
+    *reinterpret_cast<V4u*>(buf + N * lane) = *reinterpret_cast<const V4u*>(in);
+    wave_lds_sync();
+#pragma unroll
+    for (int e = 0; e < N; ++e) out[e] = buf[lane + 64 * e];
+    wave_lds_sync();
+}
+template <typename T, int N>
+__device__ __forceinline__ void lanes_to_units(T* buf, int lane, const T in[N], T out[N])
+{
+#pragma unroll
+    for (int e = 0; e < N; ++e) buf[lane + 64 * e] = in[e];
+    wave_lds_sync();
+    *reinterpret_cast<V4u*>(out) = *reinterpret_cast<const V4u*>(buf + N * lane);
+    wave_lds_sync();
+}
+
+// Unit-wise side buffer access at positions j0 .. j0 + N - 1, bounded by
+// `length` (a tile may end inside a unit); 16-byte vectors when VEC and the
+// unit is whole.
+template <typename T, bool VEC, int N>
+__device__ __forceinline__ void load_unit(const T* p, int64_t j0, int64_t length, T v[N])
+{
+    if (VEC && j0 + N <= length) {
+        if (sizeof(T) * N == 16) {
+            load_vec<T>(p + j0, v);
+        } else {
+            load_f32s<N>(reinterpret_cast<const float*>(p) + j0, reinterpret_cast<float*>(v));
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e) v[e] = j0 + e < length ? p[j0 + e] : T(0);
+    }
+}
+template <typename T, bool VEC, int N>
+__device__ __forceinline__ void store_unit(T* p, int64_t j0, int64_t length, const T v[N])
+{
+    if (VEC && j0 + N <= length) {
+        if (sizeof(T) * N == 16) {
+            store_vec<T>(p + j0, v);
+        } else {
+            store_f32s<N>(reinterpret_cast<float*>(p) + j0, reinterpret_cast<const float*>(v));
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e)
+            if (j0 + e < length) p[j0 + e] = v[e];
+    }
+}
+
+// Perturbation through a map (see k_perturb for the arithmetic).
+template <typename T, int AUX, bool VEC, int ADDR>
+__global__ __launch_bounds__(kBlock) void k_perturb_map(StreamArgs a)
+{
+    constexpr int N = UnitOf<T>::n;
+    const BmTables* tb = stage_bm_tables<kBlock>();
+    __shared__ __attribute__((aligned(16))) T xch[kBlock / 64][64 * N];
+    const int lane = threadIdx.x & 63;
+    T* buf = xch[threadIdx.x / 64];
+    T* w = static_cast<T*>(a.w);
+    const int64_t tiles = (a.length + 64 * N - 1) / (64 * N);
+    for (int64_t t = wave_id(); t < tiles; t += wave_count()) {
+        const int64_t t0 = t * 64 * N, j0 = t0 + (int64_t)N * lane;
+        int64_t idx[N];
+        const bool all_valid = tile_entries<ADDR, N>(a.index, a.offset, a.length, a.numel, t0, lane, idx);
+        float src[N];
+        if (AUX == kAuxMaster) {
+            load_unit<float, VEC, N>(static_cast<const float*>(a.aux), j0, a.length, src);
+        } else {
+            T old[N];
+            if (AUX == kAuxBackup) {
+                load_unit<T, VEC, N>(static_cast<const T*>(a.aux), j0, a.length, old);
+            } else {
+                T g[N];
+                gather_lanes<T, N>(w, idx, all_valid, g);
+                lanes_to_units<T, N>(buf, lane, g, old);
+                if (AUX == kAuxSnapshot) store_unit<T, VEC, N>(static_cast<T*>(a.aux), j0, a.length, old);
+            }
+#pragma unroll
+            for (int e = 0; e < N; ++e) src[e] = to_f32<T>(old[e]);
+        }
+        float z[N];
+        unit_normals<N>(a.k0, a.k1, (uint64_t)(a.noise0 + j0) >> 2, tb, z);
+        T out[N], v[N];
+#pragma unroll
+        for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.scale, z[e], src[e]));
+        units_to_lanes<T, N>(buf, lane, out, v);
+        scatter_lanes<T, N>(w, idx, all_valid, v);
+    }
+}
+
+// Copies through a map, all lane-interleaved (no noise, no exchange):
+// KIND 0: w[p(j)] = aux[j] (restore from the backup);
+// KIND 1: aux[j] = w[p(j)] (backup; skipped entries give 0);
+// KIND 2: w[p(j)] = rne_bf16(master[j]) (restore from a master);
+// KIND 3: master[j] = f32(w[p(j)]) (master staging).
+constexpr int kCopyRestore = 0, kCopyBackup = 1, kCopyRestoreMaster = 2, kCopyStageMaster = 3;
+
+template <typename T, int KIND, bool NT, int ADDR>
+__global__ __launch_bounds__(kBlock) void k_copy_map(StreamArgs a)
+{
+    constexpr int N = UnitOf<T>::n;
+    const int lane = threadIdx.x & 63;
+    T* w = static_cast<T*>(a.w);
+    const int64_t tiles = (a.length + 64 * N - 1) / (64 * N);
+    for (int64_t t = wave_id(); t < tiles; t += wave_count()) {
+        const int64_t t0 = t * 64 * N;
+        int64_t idx[N];
+        const bool all_valid = tile_entries<ADDR, N>(a.index, a.offset, a.length, a.numel, t0, lane, idx);
+        const bool full = t0 + 64 * N <= a.length;
+        if (KIND == kCopyRestore || KIND == kCopyRestoreMaster) {
+            T v[N];
+#pragma unroll
+            for (int e = 0; e < N; ++e) {
+                const int64_t j = t0 + lane + 64 * e;
+                if (KIND == kCopyRestore) {
+                    const T* snap = static_cast<const T*>(a.aux);
+                    v[e] = full || j < a.length ? (NT ? __builtin_nontemporal_load(snap + j) : snap[j]) : T(0);
+                } else {
+                    const float* master = static_cast<const float*>(a.aux);
+                    const float m = full || j < a.length ? (NT ? __builtin_nontemporal_load(master + j) : master[j])
+                                                        : 0.0f;
+                    v[e] = from_f32<T>(m);
+                }
+            }
+            scatter_lanes<T, N>(w, idx, all_valid, v);
+        } else {
+            T v[N];
+            gather_lanes<T, N>(w, idx, all_valid, v);
+#pragma unroll
+            for (int e = 0; e < N; ++e) {
+                const int64_t j = t0 + lane + 64 * e;
+                if (!full && j >= a.length) continue;
+                if (KIND == kCopyBackup) {
+                    T* backup = static_cast<T*>(a.aux);
+                    if (NT) __builtin_nontemporal_store(v[e], backup + j);
+                    else backup[j] = v[e];
+                } else {
+                    float* master = static_cast<float*>(a.aux);
+                    if (NT) __builtin_nontemporal_store(to_f32<T>(v[e]), master + j);
+                    else master[j] = to_f32<T>(v[e]);
+                }
+            }
+        }
+    }
+}
+
+// Update through a map (see k_update for the arithmetic).
+template <typename T, bool MASTER, bool VEC, int ADDR>
+__global__ __launch_bounds__(kBlock) void k_update_map(UpdateArgs a)
+{
+    constexpr int N = UnitOf<T>::n;   // a master update has bf16 weights: N = 8
+    const BmTables* tb = stage_bm_tables<kBlock>();
+    __shared__ float coef[kMaxMembers];
+    __shared__ __attribute__((aligned(16))) T xch[kBlock / 64][64 * N];
+    fold_coefficients(a.n_members, a.n_streams, a.member_stream, a.member_sign, a.rnorm, coef);
+    const int lane = threadIdx.x & 63;
+    T* buf = xch[threadIdx.x / 64];
+    T* w = static_cast<T*>(a.w);
+    const int64_t tiles = (a.length + 64 * N - 1) / (64 * N);
+    for (int64_t t = wave_id(); t < tiles; t += wave_count()) {
+        const int64_t t0 = t * 64 * N, j0 = t0 + (int64_t)N * lane;
+        int64_t idx[N];
+        const bool all_valid = tile_entries<ADDR, N>(a.index, a.offset, a.length, a.numel, t0, lane, idx);
+        T g[N];
+        if (!MASTER) gather_lanes<T, N>(w, idx, all_valid, g);   // in flight while the noise is generated
+        float acc[N];
+        accumulate_streams<N>(a.seed_lo, a.seed_hi, coef, 0, a.n_streams, (uint64_t)(a.noise0 + j0) >> 2, tb, acc);
+        T out[N], v[N];
+        if (MASTER) {
+            float m[N];
+            load_unit<float, VEC, N>(a.master, j0, a.length, m);
+#pragma unroll
+            for (int e = 0; e < N; ++e) {
+                m[e] = __builtin_fmaf(a.step, acc[e], m[e]);
+                out[e] = from_f32<T>(m[e]);
+            }
+            store_unit<float, VEC, N>(a.master, j0, a.length, m);
+        } else {
+            T old[N];
+            lanes_to_units<T, N>(buf, lane, g, old);
+#pragma unroll
+            for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(a.step, acc[e], to_f32<T>(old[e])));
+        }
+        units_to_lanes<T, N>(buf, lane, out, v);
+        scatter_lanes<T, N>(w, idx, all_valid, v);
+    }
 }
 
 // ------------------------------------------------------------ step update --
 // theta += sum_k P_k step_k sum_{u in streams of k} c_u eps_u (Eq. 13, Alg. 1):
 // every subspace of the partition with its own members, in one launch.  Units
 // restart at each subspace's first position, so noise position j is always
-// relative to the subspace; each wave works on 64 units of one subspace.
+// relative to the subspace; each wave works on 64 units of one subspace (one
+// tile, taken lane-interleaved on an element map as in the map kernels).
 template <typename T, int ADDR>
 __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
 {
     constexpr int N = UnitOf<T>::n;
     const BmTables* tb = stage_bm_tables<kBlock>();
     __shared__ float coef[kMaxMembers];
-    for (int u = threadIdx.x; u < a.n_streams; u += blockDim.x) {
-        double c = 0.0;
-        for (int i = 0; i < a.n_members; ++i)
-            if (a.member_stream[i] == u) c += (double)a.member_sign[i] * (double)a.rnorm[i];
-        coef[u] = (float)c;
-    }
-    __syncthreads();
+    __shared__ __attribute__((aligned(16))) T xch[kBlock / 64][64 * N];
+    fold_coefficients(a.n_members, a.n_streams, a.member_stream, a.member_sign, a.rnorm, coef);
     T* w = static_cast<T*>(a.w);
     const int lane = threadIdx.x & 63;
-    const int64_t waves = (int64_t)gridDim.x * (kBlock / 64);
-    const int64_t wave = (int64_t)blockIdx.x * (kBlock / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+    T* buf = xch[threadIdx.x / 64];
     const int64_t tiles = a.tile_begin[a.K];
-    for (int64_t t = wave; t < tiles; t += waves) {
+    for (int64_t t = wave_id(); t < tiles; t += wave_count()) {
         // t is the same for the whole wave; so are k and the stream range, which
         // keeps the seed and coefficient reads scalar
         int k = 0;
@@ -587,39 +785,35 @@ __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
         const int st1 = __builtin_amdgcn_readfirstlane(a.stream_begin[k + 1]);
         const int64_t off = a.offset[k];
         const int64_t len = a.length[k];
-        const int64_t j0 = ((t - a.tile_begin[k]) * 64 + lane) * N;
+        const float step = a.step[k];
+        const int64_t t0 = (t - a.tile_begin[k]) * 64 * N;
+        const int64_t j0 = t0 + (int64_t)N * lane;
+        if (kMap<ADDR>) {
+            int64_t idx[N];
+            const bool all_valid = tile_entries<ADDR, N>(a.index, off, len, a.numel, t0, lane, idx);
+            T g[N], old[N], out[N], v[N];
+            gather_lanes<T, N>(w, idx, all_valid, g);
+            float acc[N];
+            accumulate_streams<N>(a.seed_lo, a.seed_hi, coef, st0, st1, (uint64_t)j0 >> 2, tb, acc);
+            lanes_to_units<T, N>(buf, lane, g, old);
+#pragma unroll
+            for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(step, acc[e], to_f32<T>(old[e])));
+            units_to_lanes<T, N>(buf, lane, out, v);
+            scatter_lanes<T, N>(w, idx, all_valid, v);
+            continue;
+        }
         if (j0 >= len) continue;
         int64_t base = 0;
         const bool vec = ((a.vec_mask >> k) & 1u) && j0 + N <= len &&
-                         (kMap<ADDR> || unit_base<ADDR>(a.index, off, a.numel, a.chunk_shift, j0, N, base));
+                         unit_base<ADDR>(a.index, off, a.numel, a.chunk_shift, j0, N, base);
         float acc[N];
-#pragma unroll
-        for (int e = 0; e < N; ++e) acc[e] = 0.0f;
-        for (int st = st0; st < st1; ++st) {
-            const float c = coef[st];
-            float z[N];
-            unit_normals<N>(a.seed_lo[st], a.seed_hi[st], (uint64_t)j0 >> 2, tb, z);
-#pragma unroll
-            for (int e = 0; e < N; ++e) acc[e] = __builtin_fmaf(c, z[e], acc[e]);
-        }
-        const float step = a.step[k];
+        accumulate_streams<N>(a.seed_lo, a.seed_hi, coef, st0, st1, (uint64_t)j0 >> 2, tb, acc);
         if (vec) {
             T v[N], out[N];
-            int64_t idx[N];
-            if (kMap<ADDR>) {
-                load_map<ADDR, N>(a.index, off + j0, idx);
-#pragma unroll
-                for (int e = 0; e < N; ++e) v[e] = (idx[e] >= 0 && idx[e] < a.numel) ? w[idx[e]] : T(0);
-            } else {
-                load_vec<T>(w + base, v);
-            }
+            load_vec<T>(w + base, v);
 #pragma unroll
             for (int e = 0; e < N; ++e) out[e] = from_f32<T>(__builtin_fmaf(step, acc[e], to_f32<T>(v[e])));
-            if (kMap<ADDR>) {
-                scatter_unit<T, N>(w, idx, out, a.numel);
-            } else {
-                store_vec<T>(w + base, out);
-            }
+            store_vec<T>(w + base, out);
         } else {
 #pragma unroll
             for (int e = 0; e < N; ++e) {
@@ -995,6 +1189,30 @@ __global__ __launch_bounds__(kBlock) void k_rng_probe(uint64_t seed, int64_t n, 
     if ((threadIdx.x & 63) == 0) atomicXor(sink, acc);
 }
 
+// Measurement references with nothing but the memory traffic.  The plainest
+// gather (DIR 0: buf[j] = w[p(j)]) or scatter (DIR 1: w[p(j)] = buf[j])
+// through an element map, one position per thread.
+template <typename T, int DIR, int ADDR>
+__global__ __launch_bounds__(kBlock) void k_probe_map_copy(StreamArgs a)
+{
+    T* w = static_cast<T*>(a.w);
+    T* buf = static_cast<T*>(a.aux);
+    for (int64_t j = global_tid(); j < a.length; j += grid_stride()) {
+        const int64_t i = map_entry<ADDR>(a.index, a.offset + j);
+        if ((uint64_t)i >= (uint64_t)a.numel) continue;
+        if (DIR == 0)
+            buf[j] = w[i];
+        else
+            w[i] = buf[j];
+    }
+}
+
+// A plain copy of n16 16-byte vectors, one per thread per iteration.
+__global__ __launch_bounds__(kBlock) void k_probe_copy(const V4u* src, V4u* dst, int64_t n16)
+{
+    for (int64_t i = global_tid(); i < n16; i += grid_stride()) dst[i] = src[i];
+}
+
 int64_t grid_for(int64_t work_items, int64_t cap = kMaxGrid)
 {
     int64_t blocks = (work_items + kBlock - 1) / kBlock;
@@ -1003,15 +1221,7 @@ int64_t grid_for(int64_t work_items, int64_t cap = kMaxGrid)
 }
 
 // Noise kernels on contiguous or chunked subspaces loop over the subspace from
-// a few workgroups per CU (the tables are staged once per workgroup).  On
-// index maps one workgroup per 256 units is faster: workgroups then start in
-// position order, so the scattered accesses in flight stay in a narrow window
-// of the weights (DRAM row and cache locality).
-inline int64_t rng_grid_cap(int addr)
-{
-    return addr == kGather || addr == kGather32 ? kMaxGrid : kRngMaxGrid;
-}
-
+// a few workgroups per CU (the tables are staged once per workgroup).
 template <typename K, typename A>
 hipError_t launch1d(K kernel, int64_t items, const A& args, hipStream_t s, int64_t cap)
 {
@@ -1025,32 +1235,51 @@ int64_t units_of(int64_t length)
     return (length + UnitOf<T>::n - 1) / UnitOf<T>::n;
 }
 
-// Instantiate a streaming kernel for the addressing mode and vector flag.
-#define CPES_DISPATCH_ADDR_VEC(KERNEL, ...)                                                          \
+// Map kernels: one wave per tile of 64 N positions, up to the grid cap; the
+// waves of a launch then start in position order, which keeps the scattered
+// accesses in flight within a narrow window of the weights.
+#ifndef CPES_MAP_GRID_CAP
+#define CPES_MAP_GRID_CAP kMaxGrid
+#endif
+template <typename T>
+int64_t map_threads(int64_t length)
+{
+    const int64_t tile = 64 * UnitOf<T>::n;
+    return (length + tile - 1) / tile * 64;
+}
+
+// Instantiate a streaming kernel for the addressing mode and vector flag;
+// element maps go to the map kernel MAPK instantiated with MARGS.
+#define CPES_DISPATCH(KERNEL, KARGS, MAPK, MARGS)                                                     \
     switch (addr) {                                                                                  \
-    case kGather: return vec ? launch1d(KERNEL<__VA_ARGS__, kGather, true>, u, a, s, cap)                  \
-                             : launch1d(KERNEL<__VA_ARGS__, kGather, false>, u, a, s, cap);                \
-    case kGather32: return vec ? launch1d(KERNEL<__VA_ARGS__, kGather32, true>, u, a, s, cap)              \
-                               : launch1d(KERNEL<__VA_ARGS__, kGather32, false>, u, a, s, cap);            \
-    case kChunk: return vec ? launch1d(KERNEL<__VA_ARGS__, kChunk, true>, u, a, s, cap)                    \
-                            : launch1d(KERNEL<__VA_ARGS__, kChunk, false>, u, a, s, cap);                  \
-    default: return vec ? launch1d(KERNEL<__VA_ARGS__, kContig, true>, u, a, s, cap)                       \
-                        : launch1d(KERNEL<__VA_ARGS__, kContig, false>, u, a, s, cap);                     \
+    case kGather: return launch1d(MAPK<MARGS, kGather>, map_threads<T>(a.length), a, s, CPES_MAP_GRID_CAP); \
+    case kGather32: return launch1d(MAPK<MARGS, kGather32>, map_threads<T>(a.length), a, s, CPES_MAP_GRID_CAP); \
+    case kChunk: return vec ? launch1d(KERNEL<KARGS, kChunk, true>, u, a, s, cap)                    \
+                            : launch1d(KERNEL<KARGS, kChunk, false>, u, a, s, cap);                  \
+    default: return vec ? launch1d(KERNEL<KARGS, kContig, true>, u, a, s, cap)                       \
+                        : launch1d(KERNEL<KARGS, kContig, false>, u, a, s, cap);                     \
     }
+#define CPES_COMMA ,
 
 template <typename T, int AUX>
 hipError_t perturb_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
-    const int64_t u = units_of<T>(a.length), cap = rng_grid_cap(addr);
-    CPES_DISPATCH_ADDR_VEC(k_perturb, T, AUX)
+    const int64_t u = units_of<T>(a.length), cap = kRngMaxGrid;
+    if (vec) {
+        CPES_DISPATCH(k_perturb, T CPES_COMMA AUX, k_perturb_map, T CPES_COMMA AUX CPES_COMMA true)
+    }
+    CPES_DISPATCH(k_perturb, T CPES_COMMA AUX, k_perturb_map, T CPES_COMMA AUX CPES_COMMA false)
 }
 
 template <typename T, bool MASTER>
 hipError_t update_t(int addr, bool vec, const UpdateArgs& a, hipStream_t s)
 {
-    const int64_t u = (a.length + (MASTER ? 8 : UnitOf<T>::n) - 1) / (MASTER ? 8 : UnitOf<T>::n),
-                  cap = rng_grid_cap(addr);
-    CPES_DISPATCH_ADDR_VEC(k_update, T, MASTER)
+    constexpr int N = MASTER ? 8 : UnitOf<T>::n;
+    const int64_t u = (a.length + N - 1) / N, cap = kRngMaxGrid;
+    if (vec) {
+        CPES_DISPATCH(k_update, T CPES_COMMA MASTER, k_update_map, T CPES_COMMA MASTER CPES_COMMA true)
+    }
+    CPES_DISPATCH(k_update, T CPES_COMMA MASTER, k_update_map, T CPES_COMMA MASTER CPES_COMMA false)
 }
 
 // Copies whose source and destination together exceed the 256 MB last-level
@@ -1067,9 +1296,9 @@ hipError_t restore_copy_t(int addr, bool vec, const StreamArgs& a, hipStream_t s
 {
     const int64_t u = units_of<T>(a.length), cap = kMaxGrid;
     if (streaming(a.length, 2 * sizeof(T))) {
-        CPES_DISPATCH_ADDR_VEC(k_restore_copy, T, true)
+        CPES_DISPATCH(k_restore_copy, T CPES_COMMA true, k_copy_map, T CPES_COMMA kCopyRestore CPES_COMMA true)
     }
-    CPES_DISPATCH_ADDR_VEC(k_restore_copy, T, false)
+    CPES_DISPATCH(k_restore_copy, T CPES_COMMA false, k_copy_map, T CPES_COMMA kCopyRestore CPES_COMMA false)
 }
 
 template <typename T>
@@ -1077,9 +1306,9 @@ hipError_t backup_copy_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
     const int64_t u = units_of<T>(a.length), cap = kMaxGrid;
     if (streaming(a.length, 2 * sizeof(T))) {
-        CPES_DISPATCH_ADDR_VEC(k_backup_copy, T, true)
+        CPES_DISPATCH(k_backup_copy, T CPES_COMMA true, k_copy_map, T CPES_COMMA kCopyBackup CPES_COMMA true)
     }
-    CPES_DISPATCH_ADDR_VEC(k_backup_copy, T, false)
+    CPES_DISPATCH(k_backup_copy, T CPES_COMMA false, k_copy_map, T CPES_COMMA kCopyBackup CPES_COMMA false)
 }
 
 template <typename T>
@@ -1087,24 +1316,26 @@ hipError_t stage_master_t(int addr, bool vec, const StreamArgs& a, hipStream_t s
 {
     const int64_t u = units_of<T>(a.length), cap = kMaxGrid;
     if (streaming(a.length, sizeof(T) + 4)) {
-        CPES_DISPATCH_ADDR_VEC(k_stage_master, T, true)
+        CPES_DISPATCH(k_stage_master, T CPES_COMMA true, k_copy_map, T CPES_COMMA kCopyStageMaster CPES_COMMA true)
     }
-    CPES_DISPATCH_ADDR_VEC(k_stage_master, T, false)
+    CPES_DISPATCH(k_stage_master, T CPES_COMMA false, k_copy_map, T CPES_COMMA kCopyStageMaster CPES_COMMA false)
 }
 
 hipError_t restore_master_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
+    using T = uint16_t;
     const int64_t u = (a.length + 7) / 8, cap = kMaxGrid;
     if (streaming(a.length, 6)) {
-        CPES_DISPATCH_ADDR_VEC(k_restore_master, true)
+        CPES_DISPATCH(k_restore_master, true, k_copy_map, T CPES_COMMA kCopyRestoreMaster CPES_COMMA true)
     }
-    CPES_DISPATCH_ADDR_VEC(k_restore_master, false)
+    CPES_DISPATCH(k_restore_master, false, k_copy_map, T CPES_COMMA kCopyRestoreMaster CPES_COMMA false)
 }
 
 template <typename T>
 hipError_t update_step_t(int addr, const StepArgs& a, hipStream_t s)
 {
-    const int64_t blocks = grid_for(a.tile_begin[a.K] * 64, rng_grid_cap(addr));
+    const bool map = addr == kGather || addr == kGather32;
+    const int64_t blocks = grid_for(a.tile_begin[a.K] * 64, map ? CPES_MAP_GRID_CAP : kRngMaxGrid);
     switch (addr) {
     case kGather: hipLaunchKernelGGL((k_update_step<T, kGather>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
     case kGather32: hipLaunchKernelGGL((k_update_step<T, kGather32>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
@@ -1230,6 +1461,35 @@ hipError_t launch_rng_probe(uint64_t seed, int64_t n, uint32_t* sink, hipStream_
     const int64_t blocks = grid_for((n + 7) / 8) < 8192 ? grid_for((n + 7) / 8) : 8192;
     hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(1), 0, s, sink);
     hipLaunchKernelGGL(k_rng_probe, dim3((unsigned)blocks), dim3(kBlock), 0, s, seed, n, sink);
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_map_copy(int dtype, int addr, int direction, const StreamArgs& a, hipStream_t s)
+{
+    const int64_t g = grid_for(a.length);
+#define CPES_PROBE(T, D, A) hipLaunchKernelGGL((k_probe_map_copy<T, D, A>), dim3((unsigned)g), dim3(kBlock), 0, s, a)
+    if (dtype == 0) {
+        if (addr == kGather32) {
+            if (direction == 0) CPES_PROBE(uint16_t, 0, kGather32); else CPES_PROBE(uint16_t, 1, kGather32);
+        } else {
+            if (direction == 0) CPES_PROBE(uint16_t, 0, kGather); else CPES_PROBE(uint16_t, 1, kGather);
+        }
+    } else {
+        if (addr == kGather32) {
+            if (direction == 0) CPES_PROBE(float, 0, kGather32); else CPES_PROBE(float, 1, kGather32);
+        } else {
+            if (direction == 0) CPES_PROBE(float, 0, kGather); else CPES_PROBE(float, 1, kGather);
+        }
+    }
+#undef CPES_PROBE
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_copy(const void* src, void* dst, int64_t bytes, hipStream_t s)
+{
+    const int64_t n16 = bytes / 16;
+    hipLaunchKernelGGL(k_probe_copy, dim3((unsigned)grid_for(n16)), dim3(kBlock), 0, s,
+                       static_cast<const V4u*>(src), static_cast<V4u*>(dst), n16);
     return hipGetLastError();
 }
 

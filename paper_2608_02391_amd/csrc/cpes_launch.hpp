@@ -9,7 +9,8 @@ namespace cpes {
 
 constexpr int kBlock = 256;             // threads per workgroup for streaming kernels
 constexpr int64_t kMaxGrid = 1 << 20;   // workgroups per launch; larger jobs loop
-// Workgroups per launch of the noise kernels, which stage a 4 KiB table in
+// Workgroups per launch of the noise kernels on contiguous and chunked
+// subspaces, which stage the 12 KiB Box-Muller tables (sizeof(BmTables)) in
 // LDS per workgroup: a few per CU, each looping over many units.
 constexpr int64_t kRngMaxGrid = 8192;
 
@@ -132,5 +133,7 @@ hipError_t launch_debug_bm_grid(uint32_t m0, int64_t n, double* rho, double* c, 
 hipError_t launch_debug_prp(uint64_t seed, int64_t d, int32_t K, int32_t half_bits, int64_t i0, int64_t n,
                             int64_t* perm, int32_t* bucket, hipStream_t s);
 hipError_t launch_rng_probe(uint64_t seed, int64_t n, uint32_t* sink, hipStream_t s);
+hipError_t launch_probe_map_copy(int dtype, int addr, int direction, const StreamArgs& a, hipStream_t s);
+hipError_t launch_probe_copy(const void* src, void* dst, int64_t bytes, hipStream_t s);
 
 }  // namespace cpes

@@ -37,7 +37,7 @@ def test_header_declares_the_boundary():
 def test_library_exports_every_declared_symbol(lib):
     for name in _declared():
         assert hasattr(lib, name), name
-    assert lib.cpes_abi_version() == 5
+    assert lib.cpes_abi_version() == 6
 
 
 def _sub(offset=0, length=16, index=None, chunk=0, index32=None, noise_offset=0):
@@ -296,3 +296,23 @@ def test_binding_checks_buffer_sizes_and_dtypes(lib):
                           workspace=torch.zeros(16, dtype=torch.uint8))
     with pytest.raises(ValueError, match="bounds needs K"):
         cp.cpes_partition(cp.PART_CONTIGUOUS, 100, 4, bounds=[0, 50, 100])
+
+
+def test_probes_reject_bad_arguments(lib):
+    s = _sub(length=16, index=FAKE)
+    plain = _sub(length=16)
+    chunked = _sub(length=16, index=FAKE, chunk=8)
+    cases = [
+        (FAKE, 64, cp.BF16, ctypes.byref(plain), FAKE, 0),     # no element map
+        (FAKE, 64, cp.BF16, ctypes.byref(chunked), FAKE, 0),   # chunk lists are not element maps
+        (FAKE, 64, cp.BF16, ctypes.byref(s), None, 1),         # null buffer
+        (FAKE, 64, cp.BF16, ctypes.byref(s), FAKE, 2),         # direction
+        (None, 64, cp.BF16, ctypes.byref(s), FAKE, 0),         # null weights
+    ]
+    for args in cases:
+        rc, msg = _rc_msg(lib, lib.cpes_probe_map_copy(*args, None))
+        assert rc == cp.ERR_INVALID_ARGUMENT, (args, msg)
+    for src, dst, n in ((None, FAKE, 16), (FAKE, None, 16), (FAKE, FAKE, 15), (FAKE, FAKE, -16), (FAKE + 8, FAKE, 16)):
+        rc, msg = _rc_msg(lib, lib.cpes_probe_copy(src, dst, n, None))
+        assert rc == cp.ERR_INVALID_ARGUMENT, (src, dst, n, msg)
+    assert lib.cpes_probe_copy(FAKE, FAKE, 0, None) == cp.OK
