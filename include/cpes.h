@@ -86,6 +86,7 @@ enum cpes_scale_mode { CPES_SCALE_ALPHA_OVER_N_SIGMA = 0, CPES_SCALE_ALPHA_OVER_
 #define CPES_MAX_GROUPS 1024         /* reward groups per cpes_normalize_rewards call */
 #define CPES_MAX_PERMUTATION_K 256   /* subspaces of a CPES_PART_PERMUTATION partition */
 #define CPES_MAX_STEP_SUBSPACES 32   /* subspaces per cpes_update_step call */
+#define CPES_STATIC_MAX_CHUNKS (1 << 20) /* chunks per cpes_partition_chunks_static call */
 
 typedef struct cpes_subspace {
     int64_t offset;          /* first parameter (no map) or first map entry */
@@ -168,6 +169,28 @@ CPES_API int cpes_partition_chunks(int64_t d, int64_t chunk, int32_t K, uint64_t
                                    int64_t* list_offsets_host, int64_t* lengths_host, int64_t* chunks_dev,
                                    void* workspace_dev, size_t workspace_bytes, int32_t* status_dev,
                                    void* stream);
+
+/*
+ * cpes_partition_chunks_static -- cpes_partition_chunks with no workspace
+ * argument and no allocation of any kind, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Its scratch space is a file-scope device array of
+ * the library (2,621,696 bytes: room for n_chunks <= CPES_STATIC_MAX_CHUNKS
+ * and K <= CPES_MAX_PERMUTATION_K), which every GPU the library runs on holds
+ * until the process ends.  The first call on a device looks up that device's
+ * copy (hipGetSymbolAddress; not a stream operation, so make that first call
+ * outside a graph capture).  All calls on one GPU share the array and each
+ * leaves its contents behind: calls that overlap in time on one GPU (other
+ * streams or threads) race and must be serialised by the caller.  Nothing in
+ * it needs to start at zero: every call writes each scratch entry before
+ * reading it.
+ * Arguments, outputs and results as cpes_partition_chunks (bit-identical).
+ * Errors: as cpes_partition_chunks; more than CPES_STATIC_MAX_CHUNKS chunks
+ *   -> CPES_ERR_UNSUPPORTED; the address lookup failing -> CPES_ERR_HIP.
+ */
+CPES_API int cpes_partition_chunks_static(int64_t d, int64_t chunk, int32_t K, uint64_t seed,
+                                          int64_t* list_offsets_host, int64_t* lengths_host, int64_t* chunks_dev,
+                                          int32_t* status_dev, void* stream);
 
 /* Workspace bytes cpes_partition_chunks needs; 0 for invalid arguments. */
 CPES_API size_t cpes_partition_chunks_workspace_bytes(int64_t d, int64_t chunk, int32_t K);

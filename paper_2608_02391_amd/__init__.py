@@ -25,7 +25,7 @@ MAX_MEMBERS, MAX_REWARDS, MAX_GROUPS, MAX_PERMUTATION_K, MAX_STEP_SUBSPACES = 25
 
 EXPORTED = (
     "cpes_partition", "cpes_partition32", "cpes_partition_workspace_bytes", "cpes_partition_chunks",
-    "cpes_partition_chunks_workspace_bytes", "cpes_perturb", "cpes_restore", "cpes_backup",
+    "cpes_partition_chunks_workspace_bytes", "cpes_partition_chunks_static", "cpes_perturb", "cpes_restore", "cpes_backup",
     "cpes_backup_to_host", "cpes_restore_from_host", "cpes_stage_master", "cpes_normalize_rewards",
     "cpes_update", "cpes_update_step", "cpes_update_step32", "cpes_debug_philox", "cpes_debug_normals", "cpes_debug_bm_grid",
     "cpes_debug_prp", "cpes_rng_probe", "cpes_probe_map_copy", "cpes_probe_copy", "cpes_fill_normal",
@@ -64,6 +64,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "cpes_partition_workspace_bytes": [i32, i64, i32],
         "cpes_partition_chunks": [i64, i64, i32, u64, vp, vp, vp, vp, ctypes.c_size_t, vp, vp],
         "cpes_partition_chunks_workspace_bytes": [i64, i64, i32],
+        "cpes_partition_chunks_static": [i64, i64, i32, u64, vp, vp, vp, vp, vp],
         "cpes_perturb": [vp, i64, i32, sp, f32, u64, i32, vp, i32, vp],
         "cpes_restore": [vp, i64, i32, sp, f32, u64, i32, vp, i32, vp],
         "cpes_backup": [vp, i64, i32, sp, vp, vp],
@@ -256,6 +257,19 @@ def cpes_partition_chunks(d: int, chunk: int, K: int, seed: int, chunks, workspa
     _check(L.cpes_partition_chunks(d, chunk, K, seed, offs, lens, _dev_ptr(chunks, "chunks"),
                                    _dev_ptr(workspace, "workspace"), ws_bytes, _dev_ptr(status, "status"),
                                    _stream(stream)))
+    return [int(x) for x in offs], [int(x) for x in lens]
+
+
+def cpes_partition_chunks_static(d: int, chunk: int, K: int, seed: int, chunks, status=None, stream=None):
+    """cpes_partition_chunks on the library's own device scratch array (no
+    workspace, no allocation); returns (list_offsets[K+1], lengths[K])."""
+    L = load()
+    offs = (ctypes.c_int64 * (K + 1))()
+    lens = (ctypes.c_int64 * K)()
+    _need(chunks, "chunks", -(-d // chunk) if chunk > 0 else 0, _torch().int64)
+    _need(status, "status", 1, _torch().int32)
+    _check(L.cpes_partition_chunks_static(d, chunk, K, seed, offs, lens, _dev_ptr(chunks, "chunks"),
+                                          _dev_ptr(status, "status"), _stream(stream)))
     return [int(x) for x in offs], [int(x) for x in lens]
 
 

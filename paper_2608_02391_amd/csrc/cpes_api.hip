@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "cpes_launch.hpp"
@@ -183,14 +184,14 @@ struct PartitionLayout {
     size_t off_counts, off_pos, off_block_sums, total;
 };
 
-size_t round_up(size_t x, size_t a)
+constexpr size_t round_up(size_t x, size_t a)
 {
     return (x + a - 1) / a * a;
 }
 
-PartitionLayout partition_layout(int64_t d, int32_t K)
+constexpr PartitionLayout partition_layout(int64_t d, int32_t K)
 {
-    PartitionLayout L;
+    PartitionLayout L{};
     L.n_tiles = (d + cpes::kTile - 1) / cpes::kTile;
     L.n_counts = (int64_t)K * L.n_tiles;
     L.scan_blocks = (L.n_counts + cpes::kScanChunk - 1) / cpes::kScanChunk;
@@ -200,6 +201,46 @@ PartitionLayout partition_layout(int64_t d, int32_t K)
     L.total = round_up(L.off_block_sums + (size_t)L.scan_blocks * 8, 256);
     return L;
 }
+
+// ------------------------------------------ allocation-free chunk partition --
+// cpes_partition_chunks_static takes its workspace from this file-scope device
+// array instead of a caller's buffer, sized for the largest partition it
+// accepts.  Each GPU holds its own copy until the process ends; host code
+// never passes the array's name to a kernel (on the host it is only a
+// stand-in symbol) but the device address that hipGetSymbolAddress returns,
+// looked up once per device on the first call there.
+constexpr size_t kStaticScratchBytes = partition_layout(CPES_STATIC_MAX_CHUNKS, CPES_MAX_PERMUTATION_K).total;
+static_assert(kStaticScratchBytes == 2621696, "the size include/cpes.h states");
+static __device__ __attribute__((aligned(256))) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices];   // device address of `scratch` on each device, once looked up
+
+int static_scratch(void** ws, const char* fn)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e, fn);
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(CPES_ERR_UNSUPPORTED, "%s: device %d beyond the %d the library tracks", fn, dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_status(e, fn);
+        if (!p || !aligned16(p)) return fail(CPES_ERR_HIP, "%s: no usable device address for the static workspace", fn);
+        g_scratch_ptr[dev] = p;
+    }
+    *ws = g_scratch_ptr[dev];
+    return CPES_OK;
+}
+
+int check_chunk_partition(int64_t d, int64_t chunk, int32_t K, const int64_t* list_offsets_host,
+                          const int64_t* lengths_host, const char* fn);
+int chunk_partition(int64_t d, int64_t chunk, int32_t K, uint64_t seed, int64_t* list_offsets_host,
+                    int64_t* lengths_host, int64_t* chunks_dev, void* workspace_dev, size_t workspace_bytes,
+                    int32_t* status_dev, void* stream, const char* fn);
 
 // The keyed-permutation partition into an int64 or a uint32 map.
 int permutation_partition(int64_t d, int32_t K, uint64_t seed, int64_t* offsets_host, int64_t* index64,
@@ -350,6 +391,37 @@ int cpes_partition_chunks(int64_t d, int64_t chunk, int32_t K, uint64_t seed, in
 {
     g_error.clear();
     const char* fn = "cpes_partition_chunks";
+    int rc = check_chunk_partition(d, chunk, K, list_offsets_host, lengths_host, fn);
+    if (rc) return rc;
+    return chunk_partition(d, chunk, K, seed, list_offsets_host, lengths_host, chunks_dev, workspace_dev,
+                           workspace_bytes, status_dev, stream, fn);
+}
+
+int cpes_partition_chunks_static(int64_t d, int64_t chunk, int32_t K, uint64_t seed, int64_t* list_offsets_host,
+                                 int64_t* lengths_host, int64_t* chunks_dev, int32_t* status_dev, void* stream)
+{
+    g_error.clear();
+    const char* fn = "cpes_partition_chunks_static";
+    int rc = check_chunk_partition(d, chunk, K, list_offsets_host, lengths_host, fn);
+    if (rc) return rc;
+    const int64_t n_chunks = (d + chunk - 1) / chunk;
+    if (n_chunks > CPES_STATIC_MAX_CHUNKS || K > CPES_MAX_PERMUTATION_K)
+        return fail(CPES_ERR_UNSUPPORTED, "%s: %lld chunks and K %d exceed the static workspace (at most %d chunks, "
+                    "K <= %d); use cpes_partition_chunks with a workspace", fn, (long long)n_chunks, K,
+                    CPES_STATIC_MAX_CHUNKS, CPES_MAX_PERMUTATION_K);
+    void* ws = nullptr;
+    if ((rc = static_scratch(&ws, fn))) return rc;
+    return chunk_partition(d, chunk, K, seed, list_offsets_host, lengths_host, chunks_dev, ws, kStaticScratchBytes,
+                           status_dev, stream, fn);
+}
+
+}  // extern "C"
+
+namespace {
+
+int check_chunk_partition(int64_t d, int64_t chunk, int32_t K, const int64_t* list_offsets_host,
+                          const int64_t* lengths_host, const char* fn)
+{
     if (d < 1 || d >= ((int64_t)1 << 62)) return fail(CPES_ERR_INVALID_ARGUMENT, "%s: d %lld out of range", fn, (long long)d);
     if (chunk < 8 || chunk > ((int64_t)1 << 30) || (chunk & (chunk - 1)) != 0)
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: chunk %lld is not a power of two in [8, 2^30]", fn, (long long)chunk);
@@ -357,6 +429,15 @@ int cpes_partition_chunks(int64_t d, int64_t chunk, int32_t K, uint64_t seed, in
     const int64_t n_chunks = (d + chunk - 1) / chunk;
     if (K < 1 || (int64_t)K > n_chunks)
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: K %d not in [1, %lld chunks]", fn, K, (long long)n_chunks);
+    return CPES_OK;
+}
+
+// The chunk partition after argument checks, on the given workspace.
+int chunk_partition(int64_t d, int64_t chunk, int32_t K, uint64_t seed, int64_t* list_offsets_host,
+                    int64_t* lengths_host, int64_t* chunks_dev, void* workspace_dev, size_t workspace_bytes,
+                    int32_t* status_dev, void* stream, const char* fn)
+{
+    const int64_t n_chunks = (d + chunk - 1) / chunk;
     // the chunk permutation is the permutation partition of the chunk ids
     int rc = cpes_partition(CPES_PART_PERMUTATION, n_chunks, K, seed, nullptr, list_offsets_host, chunks_dev,
                             workspace_dev, workspace_bytes, status_dev, stream);
@@ -375,6 +456,10 @@ int cpes_partition_chunks(int64_t d, int64_t chunk, int32_t K, uint64_t seed, in
     }
     return CPES_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 int cpes_perturb(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, float sigma, uint64_t seed,
                  int32_t sign, void* aux_dev, int aux_mode, void* stream)

@@ -316,3 +316,16 @@ def test_probes_reject_bad_arguments(lib):
         rc, msg = _rc_msg(lib, lib.cpes_probe_copy(src, dst, n, None))
         assert rc == cp.ERR_INVALID_ARGUMENT, (src, dst, n, msg)
     assert lib.cpes_probe_copy(FAKE, FAKE, 0, None) == cp.OK
+
+
+def test_static_chunk_partition_rejects_before_any_gpu_call(lib):
+    offs = (ctypes.c_int64 * 9)()
+    lens = (ctypes.c_int64 * 8)()
+    call = lambda d, chunk, K, o=offs, l=lens: lib.cpes_partition_chunks_static(d, chunk, K, 1, o, l, FAKE, None, None)
+    assert call(0, 8, 1) == cp.ERR_INVALID_ARGUMENT                  # d < 1
+    assert call(1 << 20, 12, 4) == cp.ERR_INVALID_ARGUMENT           # chunk not a power of two
+    assert call(64, 8, 9) == cp.ERR_INVALID_ARGUMENT                 # K above the chunk count
+    assert call(64, 8, 4, None) == cp.ERR_INVALID_ARGUMENT           # null host outputs
+    rc = call((1 << 23) + 8, 8, 4)                                   # 2^20 + 1 chunks: beyond the static array
+    assert rc == cp.ERR_UNSUPPORTED
+    assert "static workspace" in lib.cpes_last_error().decode()
