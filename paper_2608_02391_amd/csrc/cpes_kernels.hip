@@ -827,32 +827,78 @@ __global__ __launch_bounds__(kBlock) void k_update_step(StepArgs a)
 }
 
 // -------------------------------------------------------------- normalise --
-// One workgroup.  Group statistics are summed in fp64 in index order (one
-// thread per group), exactly as the definition reads; ranks count smaller and
-// equal rewards of the same group.
-constexpr int kNormThreads = 256;
+// One workgroup.  The rewards are sorted in LDS by the 64-bit key
+// (group, value, index) -- the value as an order-preserving 32-bit image of
+// the fp32 bits, -0 taken as +0 -- with a bitonic network.  Each group is
+// then one run of the sorted keys, in a canonical order (ascending value).
+// Z: one wave per group sums the run in fp64 (lane l takes run entries
+// l, l + 64, ... in order, then an xor-shuffle butterfly combines the 64
+// partial sums; every lane ends with the same total), for the mean and then
+// for the squared deviations.  RANK: the rank of an entry is the start of
+// its run of equal values within its group, the number of ties the run's
+// length, both found by binary search.
+constexpr int kNormThreads = 1024;
 constexpr int kNormMaxN = 4096;
 constexpr int kNormMaxGroups = 1024;
+constexpr int kNormIdxBits = 12;                 // index < kNormMaxN
+constexpr int kNormValShift = kNormIdxBits;      // value bits 12 .. 43
+constexpr int kNormGroupShift = kNormIdxBits + 32;   // group bits 44 .. 53
+static_assert((1 << kNormIdxBits) >= kNormMaxN && kNormMaxGroups <= (1 << (64 - kNormGroupShift - 1)),
+              "index, value and group fit the sort key");
+
+__device__ __forceinline__ uint32_t order_bits(float v)
+{
+    uint32_t u = __float_as_uint(v == 0.0f ? 0.0f : v);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float from_order_bits(uint32_t o)
+{
+    return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
+}
+
+// First position p in [0, n) with keys[p] >= x (keys ascending).
+__device__ __forceinline__ int lower_bound_u64(const uint64_t* keys, int n, uint64_t x)
+{
+    int lo = 0, hi = n;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (keys[mid] < x)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ double wave_sum(double x)
+{
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1) x += __shfl_xor(x, m, 64);
+    return x;
+}
 
 __global__ __launch_bounds__(kNormThreads) void k_normalize(NormalizeArgs a)
 {
 #pragma clang fp contract(off)
-    __shared__ float r[kNormMaxN];
-    __shared__ int32_t g[kNormMaxN];
-    __shared__ double mu[kNormMaxGroups];
-    __shared__ double sd[kNormMaxGroups];
-    __shared__ int32_t cnt[kNormMaxGroups];
+    __shared__ uint64_t keys[kNormMaxN];
+    __shared__ int32_t start[kNormMaxGroups + 1];
     __shared__ int bad;
     if (threadIdx.x == 0) bad = 0;
     __syncthreads();
+    int n2 = 1;
+    while (n2 < a.n) n2 <<= 1;
     int my_bad = 0;
-    for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
-        const float v = a.r[i];
-        const int32_t gi = a.group ? a.group[i] : 0;
-        r[i] = v;
-        g[i] = gi;
-        if (!__builtin_isfinite(v)) my_bad |= 1;
-        if (gi < 0 || gi >= a.n_groups) my_bad |= 2;
+    for (int i = threadIdx.x; i < n2; i += blockDim.x) {
+        uint64_t key = ~0ull;                              // padding sorts last
+        if (i < a.n) {
+            const float v = a.r[i];
+            const int32_t gi = a.group ? a.group[i] : 0;
+            if (!__builtin_isfinite(v)) my_bad |= 1;
+            if (gi < 0 || gi >= a.n_groups) my_bad |= 2;
+            key = ((uint64_t)(uint32_t)gi << kNormGroupShift) | ((uint64_t)order_bits(v) << kNormValShift) |
+                  (uint64_t)i;
+        }
+        keys[i] = key;
     }
     if (my_bad) atomicOr(&bad, my_bad);
     __syncthreads();
@@ -862,50 +908,62 @@ __global__ __launch_bounds__(kNormThreads) void k_normalize(NormalizeArgs a)
         if (a.status && threadIdx.x == 0) *a.status = status;
         return;
     }
-    for (int k = threadIdx.x; k < a.n_groups; k += blockDim.x) {
-        int c = 0;
-        double sum = 0.0;
-        for (int j = 0; j < a.n; ++j)
-            if (g[j] == k) {
-                sum += (double)r[j];
-                ++c;
-            }
-        cnt[k] = c;
-        if (a.mode == 0 && c > 0) {
-            const double m = sum / (double)c;
-            double ss = 0.0;
-            for (int j = 0; j < a.n; ++j)
-                if (g[j] == k) {
-                    const double dev = (double)r[j] - m;
-                    const double sq = dev * dev;
-                    ss += sq;
+    // bitonic sort, ascending
+    for (int k = 2; k <= n2; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = threadIdx.x; i < n2; i += blockDim.x) {
+                const int p = i ^ j;
+                if (p > i) {
+                    const uint64_t x = keys[i], y = keys[p];
+                    if ((x > y) == ((i & k) == 0)) {
+                        keys[i] = y;
+                        keys[p] = x;
+                    }
                 }
-            mu[k] = m;
-            sd[k] = __builtin_sqrt(ss / (double)c);
+            }
+            __syncthreads();
         }
     }
+    // group g is the run [start[g], start[g + 1])
+    for (int g = threadIdx.x; g <= a.n_groups; g += blockDim.x)
+        start[g] = lower_bound_u64(keys, a.n, (uint64_t)g << kNormGroupShift);
     __syncthreads();
-    for (int i = threadIdx.x; i < a.n; i += blockDim.x) {
-        const int k = g[i];
-        float o;
-        if (a.mode == 0) {
-            o = sd[k] > 0.0 ? (float)(((double)r[i] - mu[k]) / sd[k]) : 0.0f;
-        } else {
-            int less = 0, equal = 0;
-            for (int j = 0; j < a.n; ++j) {
-                if (g[j] != k) continue;
-                less += r[j] < r[i];
-                equal += r[j] == r[i];
+    constexpr uint64_t kIdxMask = (1ull << kNormIdxBits) - 1ull;
+    if (a.mode == 0) {
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, waves = blockDim.x >> 6;
+        for (int g = wave; g < a.n_groups; g += waves) {
+            const int s0 = start[g], s1 = start[g + 1], c = s1 - s0;
+            if (c == 0) continue;
+            double part = 0.0;
+            for (int p = s0 + lane; p < s1; p += 64)
+                part += (double)from_order_bits((uint32_t)(keys[p] >> kNormValShift));
+            const double mu = wave_sum(part) / (double)c;
+            part = 0.0;
+            for (int p = s0 + lane; p < s1; p += 64) {
+                const double dev = (double)from_order_bits((uint32_t)(keys[p] >> kNormValShift)) - mu;
+                part += dev * dev;
             }
-            const int c = cnt[k];
-            if (c == 1) {
-                o = 0.0f;
-            } else {
-                const double rank = (double)less + 0.5 * (double)(equal - 1);
-                o = (float)(rank / (double)(c - 1) - 0.5);
+            const double sd = __builtin_sqrt(wave_sum(part) / (double)c);
+            for (int p = s0 + lane; p < s1; p += 64) {
+                const int i = (int)(keys[p] & kIdxMask);
+                a.out[i] = sd > 0.0 ? (float)(((double)a.r[i] - mu) / sd) : 0.0f;
             }
         }
-        a.out[i] = o;
+    } else {
+        for (int p = threadIdx.x; p < a.n; p += blockDim.x) {
+            const uint64_t key = keys[p];
+            const int g = (int)(key >> kNormGroupShift);
+            const uint64_t first = key & ~kIdxMask;           // (group, value, index 0)
+            const int lo = lower_bound_u64(keys, a.n, first);
+            const int hi = lower_bound_u64(keys, a.n, first + (kIdxMask + 1));
+            const int c = start[g + 1] - start[g];
+            float o = 0.0f;
+            if (c > 1) {
+                const double rank = (double)(lo - start[g]) + 0.5 * (double)(hi - lo - 1);
+                o = (float)(rank / (double)(c - 1) - 0.5);
+            }
+            a.out[(int)(key & kIdxMask)] = o;
+        }
     }
     if (a.status && threadIdx.x == 0) *a.status = 0;
 }

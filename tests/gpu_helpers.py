@@ -86,3 +86,34 @@ def describe_mismatch(got, ref) -> str:
     r = ref.astype(np.float64)
     k = int(np.argmax(np.abs(g - r)))
     return f"max |diff| {abs(g[k] - r[k]):.3e} at {k}: got {g[k]!r} ref {r[k]!r}"
+
+
+def zscore_close(got, ref, r, group=None) -> bool:
+    """Z-scores of the device against the oracle's, per element:
+        |got - ref| <= ulp32(ref) + 2 (c + 8) 2^-53 ((1 + |z|) A / s + |z|),
+    with c the size, A the mean |r| and s the population standard deviation of
+    the element's group (fp64), z = ref.  The oracle sums each group
+    sequentially, the device in another fixed order (64 lane-strided partial
+    sums and a butterfly); each fp64 sum of c terms is within (c - 1) 2^-53 A c
+    of the exact one, so the means differ by at most about 2 (c + 8) 2^-53 A
+    and the deviations' relative error is about as large.  Carried through
+    (r - mu) / s that bounds the fp64 quotients' difference, and the rounding
+    to fp32 adds at most one ulp.  A group with s = 0 must give exact zeros."""
+    got = np.asarray(got, dtype=np.float64)
+    ref32 = np.asarray(ref, dtype=np.float32)
+    ref = ref32.astype(np.float64)
+    r = np.asarray(r, dtype=np.float64)
+    g = np.zeros(len(r), dtype=np.int64) if group is None else np.asarray(group)
+    bound = np.zeros(len(r))
+    for k in np.unique(g):
+        m = g == k
+        c = int(m.sum())
+        mu = r[m].mean()
+        s = np.sqrt(((r[m] - mu) ** 2).mean())
+        if s == 0:
+            continue                                     # outputs must be exactly 0
+        z = np.abs(ref[m])
+        bound[m] = 2 * (c + 8) * 2.0 ** -53 * ((1 + z) * np.abs(r[m]).mean() / s + z)
+    ulp = np.where(ref32 == 0, 2.0 ** -149, np.spacing(np.abs(ref32)).astype(np.float64))
+    ok = np.abs(got - ref) <= np.where(bound > 0, ulp + bound, 0.0)
+    return bool(np.all(ok))

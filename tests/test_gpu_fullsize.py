@@ -11,7 +11,8 @@ import pytest
 
 import paper_2608_02391_amd as cp
 import synthetic as S
-from tests.gpu_helpers import bf16_close, describe_mismatch, bf16_value, f32_close, to_host, torch, ulp_bf16
+from tests.gpu_helpers import (bf16_close, describe_mismatch, bf16_value, f32_close, to_host, torch, ulp_bf16,
+                               zscore_close)
 
 pytestmark = pytest.mark.gpu
 
@@ -91,7 +92,7 @@ def test_c3_layer_group_subspace(orc, T, big):
     rn_ref, _ = orc.normalize(r, W.norm_mode)
     cp.cpes_update(w, s, seeds, signs, rn, W.alpha, sigma, W.scale_mode)
     T.cuda.synchronize()
-    assert np.array_equal(rn.cpu().numpy(), rn_ref)
+    assert zscore_close(rn.cpu().numpy(), rn_ref, r)
     for p in wins[:4]:
         ref = before[p].copy()
         orc.update(ref, 0, WIN, seeds, signs, rn_ref, np.float32(W.alpha), np.float32(sigma), W.scale_mode, j0=p)
