@@ -396,9 +396,12 @@ CPES_API int cpes_debug_bm_grid(uint32_t m0, int64_t n, double* rho_dev, double*
 CPES_API int cpes_debug_prp(uint64_t seed, int64_t d, int32_t K, int64_t i0, int64_t n,
                    int64_t* perm_dev, int32_t* bucket_dev, void* stream);
 
-/* RNG-only throughput probe: generates n normals of stream `seed` (positions
- * 0 .. n-1) and folds them into sink_dev[0] (one uint32, overwritten) without
- * other memory traffic, to measure the generator's ALU ceiling. */
+/* RNG-only throughput probe: generates n normals (rounded up to a multiple
+ * of 128) -- positions 0 .. n/16 - 1 of each of the 16 streams seed ..
+ * seed + 15, the 16 streams of a position together as the update generates
+ * its members' noise -- and folds them into sink_dev[0] (one uint32,
+ * overwritten) without other memory traffic: the generator's throughput
+ * when nothing else runs. */
 CPES_API int cpes_rng_probe(uint64_t seed, int64_t n, uint32_t* sink_dev, void* stream);
 
 /* Measurement references for the map and copy kernels: the same memory
@@ -409,13 +412,15 @@ CPES_API int cpes_rng_probe(uint64_t seed, int64_t n, uint32_t* sink_dev, void* 
  *   s->length elements of `dtype`, device memory.  Entries outside
  *   [0, numel) are skipped.
  * cpes_probe_copy: dst[i] = src[i] over `bytes` bytes (a multiple of 16; both
- *   pointers 16-byte aligned device memory), one 16-byte vector per thread.
+ *   pointers 16-byte aligned device memory), one 16-byte vector per thread;
+ *   nontemporal != 0 takes non-temporal loads and stores (streaming past the
+ *   caches, as the library's large copies do).
  * Errors: null pointers, a subspace without an element map, direction not 0
  *   or 1, bytes negative or not a multiple of 16, misaligned pointers ->
  *   CPES_ERR_INVALID_ARGUMENT. */
 CPES_API int cpes_probe_map_copy(void* w_dev, int64_t numel, int dtype, const cpes_subspace* s, void* buf_dev,
                                  int direction, void* stream);
-CPES_API int cpes_probe_copy(const void* src_dev, void* dst_dev, int64_t bytes, void* stream);
+CPES_API int cpes_probe_copy(const void* src_dev, void* dst_dev, int64_t bytes, int nontemporal, void* stream);
 
 /* Message of the last error on the calling thread ("" if none). */
 CPES_API const char* cpes_last_error(void);

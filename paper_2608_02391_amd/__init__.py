@@ -81,7 +81,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "cpes_debug_prp": [u64, i64, i32, i64, i64, vp, vp, vp],
         "cpes_rng_probe": [u64, i64, vp, vp],
         "cpes_probe_map_copy": [vp, i64, i32, sp, vp, i32, vp],
-        "cpes_probe_copy": [vp, vp, i64, vp],
+        "cpes_probe_copy": [vp, vp, i64, i32, vp],
         "cpes_fill_normal": [vp, i64, i32, u64, u32, f32, vp],
         "cpes_last_error": [],
         "cpes_abi_version": [],
@@ -424,12 +424,14 @@ def cpes_probe_map_copy(w, s: Subspace, buf, direction: int, stream=None) -> Non
                                       _dev_ptr(buf, "buf"), direction, _stream(stream)))
 
 
-def cpes_probe_copy(src, dst, nbytes: int, stream=None) -> None:
-    """dst[:nbytes] = src[:nbytes], one 16-byte vector per thread: a measurement reference."""
+def cpes_probe_copy(src, dst, nbytes: int, nontemporal: bool = False, stream=None) -> None:
+    """dst[:nbytes] = src[:nbytes], one 16-byte vector per thread (non-temporal
+    accesses if asked): a measurement reference."""
     for t, what in ((src, "src"), (dst, "dst")):
         if t.numel() * t.element_size() < nbytes:
             raise ValueError(f"{what} holds fewer than {nbytes} bytes")
-    _check(load().cpes_probe_copy(_dev_ptr(src, "src"), _dev_ptr(dst, "dst"), nbytes, _stream(stream)))
+    _check(load().cpes_probe_copy(_dev_ptr(src, "src"), _dev_ptr(dst, "dst"), nbytes, int(bool(nontemporal)),
+                                  _stream(stream)))
 
 
 def cpes_abi_version() -> int:

@@ -838,7 +838,7 @@ int cpes_probe_map_copy(void* w_dev, int64_t numel, int dtype, const cpes_subspa
     return hip_status(cpes::launch_probe_map_copy(dtype, addr_mode(s), direction, a, (hipStream_t)stream), fn);
 }
 
-int cpes_probe_copy(const void* src_dev, void* dst_dev, int64_t bytes, void* stream)
+int cpes_probe_copy(const void* src_dev, void* dst_dev, int64_t bytes, int nontemporal, void* stream)
 {
     g_error.clear();
     const char* fn = "cpes_probe_copy";
@@ -848,7 +848,7 @@ int cpes_probe_copy(const void* src_dev, void* dst_dev, int64_t bytes, void* str
     if (!aligned16(src_dev) || !aligned16(dst_dev))
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: pointers must be 16-byte aligned", fn);
     if (bytes == 0) return CPES_OK;
-    return hip_status(cpes::launch_probe_copy(src_dev, dst_dev, bytes, (hipStream_t)stream), fn);
+    return hip_status(cpes::launch_probe_copy(src_dev, dst_dev, bytes, nontemporal != 0, (hipStream_t)stream), fn);
 }
 
 int cpes_rng_probe(uint64_t seed, int64_t n, uint32_t* sink_dev, void* stream)

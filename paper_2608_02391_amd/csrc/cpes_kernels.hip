@@ -1232,16 +1232,23 @@ __global__ void k_zero_u32(uint32_t* p)
     *p = 0u;
 }
 
-__global__ __launch_bounds__(kBlock) void k_rng_probe(uint64_t seed, int64_t n, uint32_t* sink)
+// RNG-only probe: each thread takes units of 8 positions and, like the update,
+// generates the noise of kRngProbeStreams consecutive seeds for each unit,
+// folding the bits into one word; no memory traffic but one atomic per wave.
+constexpr int kRngProbeStreams = 16;
+
+__global__ __launch_bounds__(kBlock) void k_rng_probe(uint64_t seed, int64_t units, uint32_t* sink)
 {
     const BmTables* tb = stage_bm_tables<kBlock>();
-    const int64_t units = (n + 7) / 8;
     uint32_t acc = 0;
     for (int64_t u = global_tid(); u < units; u += grid_stride()) {
-        float z[8];
-        normals8((uint32_t)seed, (uint32_t)(seed >> 32), (uint64_t)u * 2u, tb, z);
+        for (int st = 0; st < kRngProbeStreams; ++st) {
+            const uint64_t key = seed + (uint64_t)st;
+            float z[8];
+            normals8((uint32_t)key, (uint32_t)(key >> 32), (uint64_t)u * 2u, tb, z);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc ^= __float_as_uint(z[e]);
+            for (int e = 0; e < 8; ++e) acc ^= __float_as_uint(z[e]);
+        }
     }
     for (int off = 32; off > 0; off >>= 1) acc ^= __shfl_xor(acc, off);
     if ((threadIdx.x & 63) == 0) atomicXor(sink, acc);
@@ -1265,10 +1272,17 @@ __global__ __launch_bounds__(kBlock) void k_probe_map_copy(StreamArgs a)
     }
 }
 
-// A plain copy of n16 16-byte vectors, one per thread per iteration.
+// A plain copy of n16 16-byte vectors, one per thread per iteration; NT
+// takes non-temporal loads and stores.
+template <bool NT>
 __global__ __launch_bounds__(kBlock) void k_probe_copy(const V4u* src, V4u* dst, int64_t n16)
 {
-    for (int64_t i = global_tid(); i < n16; i += grid_stride()) dst[i] = src[i];
+    for (int64_t i = global_tid(); i < n16; i += grid_stride()) {
+        if (NT)
+            __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+        else
+            dst[i] = src[i];
+    }
 }
 
 int64_t grid_for(int64_t work_items, int64_t cap = kMaxGrid)
@@ -1296,9 +1310,6 @@ int64_t units_of(int64_t length)
 // Map kernels: one wave per tile of 64 N positions, up to the grid cap; the
 // waves of a launch then start in position order, which keeps the scattered
 // accesses in flight within a narrow window of the weights.
-#ifndef CPES_MAP_GRID_CAP
-#define CPES_MAP_GRID_CAP kMaxGrid
-#endif
 template <typename T>
 int64_t map_threads(int64_t length)
 {
@@ -1310,8 +1321,8 @@ int64_t map_threads(int64_t length)
 // element maps go to the map kernel MAPK instantiated with MARGS.
 #define CPES_DISPATCH(KERNEL, KARGS, MAPK, MARGS)                                                     \
     switch (addr) {                                                                                  \
-    case kGather: return launch1d(MAPK<MARGS, kGather>, map_threads<T>(a.length), a, s, CPES_MAP_GRID_CAP); \
-    case kGather32: return launch1d(MAPK<MARGS, kGather32>, map_threads<T>(a.length), a, s, CPES_MAP_GRID_CAP); \
+    case kGather: return launch1d(MAPK<MARGS, kGather>, map_threads<T>(a.length), a, s, kMaxGrid); \
+    case kGather32: return launch1d(MAPK<MARGS, kGather32>, map_threads<T>(a.length), a, s, kMaxGrid); \
     case kChunk: return vec ? launch1d(KERNEL<KARGS, kChunk, true>, u, a, s, cap)                    \
                             : launch1d(KERNEL<KARGS, kChunk, false>, u, a, s, cap);                  \
     default: return vec ? launch1d(KERNEL<KARGS, kContig, true>, u, a, s, cap)                       \
@@ -1393,7 +1404,7 @@ template <typename T>
 hipError_t update_step_t(int addr, const StepArgs& a, hipStream_t s)
 {
     const bool map = addr == kGather || addr == kGather32;
-    const int64_t blocks = grid_for(a.tile_begin[a.K] * 64, map ? CPES_MAP_GRID_CAP : kRngMaxGrid);
+    const int64_t blocks = grid_for(a.tile_begin[a.K] * 64, map ? kMaxGrid : kRngMaxGrid);
     switch (addr) {
     case kGather: hipLaunchKernelGGL((k_update_step<T, kGather>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
     case kGather32: hipLaunchKernelGGL((k_update_step<T, kGather32>), dim3((unsigned)blocks), dim3(kBlock), 0, s, a); break;
@@ -1515,10 +1526,11 @@ hipError_t launch_debug_prp(uint64_t seed, int64_t d, int32_t K, int32_t half_bi
 
 hipError_t launch_rng_probe(uint64_t seed, int64_t n, uint32_t* sink, hipStream_t s)
 {
-    // A few workgroups per CU looping over the units: one atomic per wave.
-    const int64_t blocks = grid_for((n + 7) / 8) < 8192 ? grid_for((n + 7) / 8) : 8192;
+    // a few workgroups per CU looping over the units: one atomic per wave
+    const int64_t units = (n + 8 * kRngProbeStreams - 1) / (8 * kRngProbeStreams);
+    const int64_t blocks = grid_for(units, kRngMaxGrid);
     hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(1), 0, s, sink);
-    hipLaunchKernelGGL(k_rng_probe, dim3((unsigned)blocks), dim3(kBlock), 0, s, seed, n, sink);
+    hipLaunchKernelGGL(k_rng_probe, dim3((unsigned)blocks), dim3(kBlock), 0, s, seed, units, sink);
     return hipGetLastError();
 }
 
@@ -1543,11 +1555,14 @@ hipError_t launch_probe_map_copy(int dtype, int addr, int direction, const Strea
     return hipGetLastError();
 }
 
-hipError_t launch_probe_copy(const void* src, void* dst, int64_t bytes, hipStream_t s)
+hipError_t launch_probe_copy(const void* src, void* dst, int64_t bytes, bool nontemporal, hipStream_t s)
 {
     const int64_t n16 = bytes / 16;
-    hipLaunchKernelGGL(k_probe_copy, dim3((unsigned)grid_for(n16)), dim3(kBlock), 0, s,
-                       static_cast<const V4u*>(src), static_cast<V4u*>(dst), n16);
+    const dim3 grid((unsigned)grid_for(n16)), block(kBlock);
+    if (nontemporal)
+        hipLaunchKernelGGL(k_probe_copy<true>, grid, block, 0, s, static_cast<const V4u*>(src), static_cast<V4u*>(dst), n16);
+    else
+        hipLaunchKernelGGL(k_probe_copy<false>, grid, block, 0, s, static_cast<const V4u*>(src), static_cast<V4u*>(dst), n16);
     return hipGetLastError();
 }
 

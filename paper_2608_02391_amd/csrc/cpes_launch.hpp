@@ -134,6 +134,6 @@ hipError_t launch_debug_prp(uint64_t seed, int64_t d, int32_t K, int32_t half_bi
                             int64_t* perm, int32_t* bucket, hipStream_t s);
 hipError_t launch_rng_probe(uint64_t seed, int64_t n, uint32_t* sink, hipStream_t s);
 hipError_t launch_probe_map_copy(int dtype, int addr, int direction, const StreamArgs& a, hipStream_t s);
-hipError_t launch_probe_copy(const void* src, void* dst, int64_t bytes, hipStream_t s);
+hipError_t launch_probe_copy(const void* src, void* dst, int64_t bytes, bool nontemporal, hipStream_t s);
 
 }  // namespace cpes

@@ -313,9 +313,9 @@ def test_probes_reject_bad_arguments(lib):
         rc, msg = _rc_msg(lib, lib.cpes_probe_map_copy(*args, None))
         assert rc == cp.ERR_INVALID_ARGUMENT, (args, msg)
     for src, dst, n in ((None, FAKE, 16), (FAKE, None, 16), (FAKE, FAKE, 15), (FAKE, FAKE, -16), (FAKE + 8, FAKE, 16)):
-        rc, msg = _rc_msg(lib, lib.cpes_probe_copy(src, dst, n, None))
+        rc, msg = _rc_msg(lib, lib.cpes_probe_copy(src, dst, n, 0, None))
         assert rc == cp.ERR_INVALID_ARGUMENT, (src, dst, n, msg)
-    assert lib.cpes_probe_copy(FAKE, FAKE, 0, None) == cp.OK
+    assert lib.cpes_probe_copy(FAKE, FAKE, 0, 1, None) == cp.OK
 
 
 def test_static_chunk_partition_rejects_before_any_gpu_call(lib):

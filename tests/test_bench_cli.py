@@ -28,10 +28,23 @@ def bench():
     ("c3", "restore", 4), ("c3", "update", 4), ("c3", "perturb", (6 + 29 * 4) / 30),
     ("c4", "restore", 12), ("c4", "perturb", 12 + 2 / 30), ("c4", "update", 12),
     ("c4u", "restore", 8), ("c4c", "restore", 4),
-    ("c5", "perturb", 6), ("c5", "restore", 4), ("c5", "update", 10), ("c5", "stage_master", 6), ("c5", "backup", 4),
+    ("c5", "perturb", 4), ("c5", "restore", 4), ("c5", "update", 10), ("c5", "stage_master", 6), ("c5", "backup", 4),
     ("c1", "restore", 8), ("c1", "perturb", (12 + 7 * 8) / 8),
     ("c3h", "perturb", 4), ("c3h", "backup_host", 2), ("c3h", "restore_host", 2),
 ])
 def test_bytes_per_position(bench, name, op, expected):
     import synthetic as S
     assert bench.bytes_per_position(S.workload(name), op) == pytest.approx(expected)
+
+
+def test_extras_default_to_the_other_benchmark_workloads(bench):
+    assert bench.parse([]).extras == ["c1", "c2", "c4", "c5"]
+    assert bench.parse(["--workload", "c4"]).extras == []
+    assert bench.parse(["--no-extras"]).extras == []
+    assert bench.parse(["--extras", "c1,c2"]).extras == ["c1", "c2"]
+
+
+def test_counter_figures_are_keyed_to_the_kernel_sources(bench):
+    sha = bench.sources_sha256()
+    assert len(sha) == 64
+    assert sha == bench.sources_sha256()          # a pure function of the sources
