@@ -12,8 +12,8 @@ import pytest
 
 import paper_2608_02391_amd as cp
 import synthetic as S
-from tests.gpu_helpers import (bf16_close, bf16_value, describe_mismatch, f32_close, to_dev, to_host, torch, ulp_bf16,
-                               zscore_close)
+from tests.gpu_helpers import (bf16_close, bf16_update_close, bf16_value, describe_mismatch, f32_close, to_dev, to_host,
+                               torch, ulp_bf16, update_slack, update_step_size, zscore_close)
 
 pytestmark = pytest.mark.gpu
 
@@ -66,8 +66,10 @@ def test_benchmark_config_step(orc, name, k):
     T.cuda.synchronize()
     got = to_host(dw)
     if W.dtype == S.BF16:
-        assert bf16_close(got[off:off + L], w[off:off + L]), describe_mismatch(bf16_value(got[off:off + L]),
-                                                                               bf16_value(w[off:off + L]))
+        step = update_step_size(W.alpha, sigma, W.n, W.scale_mode)
+        slack = lambda k: update_slack(orc, seeds, signs, rn_h, step, k)
+        assert bf16_update_close(got[off:off + L], w[off:off + L], slack), \
+            describe_mismatch(bf16_value(got[off:off + L]), bf16_value(w[off:off + L]))
     else:
         assert f32_close(got[off:off + L], w[off:off + L])
     outside = np.ones(W.d, dtype=bool)

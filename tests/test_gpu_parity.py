@@ -13,8 +13,8 @@ import pytest
 
 import paper_2608_02391_amd as cp
 import synthetic as S
-from tests.gpu_helpers import (bf16_close, bf16_value, describe_mismatch, f32_close, normals_within_2ulp, to_dev,
-                               zscore_close,
+from tests.gpu_helpers import (bf16_close, bf16_update_close, bf16_value, describe_mismatch, f32_close,
+                               normals_within_2ulp, to_dev, update_slack, update_step_size, zscore_close,
                                to_host, torch, ulp_bf16, ulp_f32)
 
 pytestmark = pytest.mark.gpu
@@ -493,7 +493,11 @@ def test_update_matches_oracle(orc, T, kind, layout, members):
     changed[pos] = True
     assert np.array_equal(got[~changed], w0[~changed])
     if dtype == S.BF16:
-        assert bf16_close(got, w), describe_mismatch(bf16_value(got), bf16_value(w))
+        step = update_step_size(alpha, sigma, n, scale)
+        inv = np.full(w.size, -1, dtype=np.int64)
+        inv[pos] = np.arange(length)
+        slack = lambda k: update_slack(orc, seeds, signs, rnorm, step, inv[k])
+        assert bf16_update_close(got, w, slack), describe_mismatch(bf16_value(got), bf16_value(w))
         assert np.mean(ulp_bf16(got, w) <= 1) > 0.9999
     else:
         assert f32_close(got, w), describe_mismatch(got, w)
@@ -622,9 +626,36 @@ def test_update_step_matches_oracle(orc, T, case, dtype, scale):
     _sync(T)
     got = to_host(dw)
     if dtype == S.BF16:
-        assert bf16_close(got, w), describe_mismatch(bf16_value(got), bf16_value(w))
+        slack = _step_slack(orc, d, host_offsets, index, seeds, signs, subs, rhat, 5e-4, sigmas, scale)
+        assert bf16_update_close(got, w, slack), describe_mismatch(bf16_value(got), bf16_value(w))
     else:
         assert f32_close(got, w), describe_mismatch(got, w)
+
+
+def _step_slack(orc, d, offsets, index, seeds, signs, subs, rnorm, alpha, sigmas, scale):
+    """update_slack for a whole-step update: parameter i of subspace k at noise
+    position j gets the bound of k's members and step."""
+    K = len(offsets) - 1
+    sub_of = np.full(d, -1, dtype=np.int64)
+    pos_of = np.full(d, -1, dtype=np.int64)
+    for k in range(K):
+        a, b = int(offsets[k]), int(offsets[k + 1])
+        params = index[a:b] if index is not None else np.arange(a, b)
+        sub_of[params] = k
+        pos_of[params] = np.arange(b - a)
+
+    def slack(ix):
+        out = np.zeros(len(ix))
+        for k in range(K):
+            sel = np.nonzero(sub_of[ix] == k)[0]
+            mem = [i for i in range(len(subs)) if subs[i] == k]
+            if sel.size == 0 or not mem:
+                continue
+            step = update_step_size(alpha, sigmas[k], len(mem), scale)
+            out[sel] = update_slack(orc, [seeds[i] for i in mem], [signs[i] for i in mem],
+                                    [rnorm[i] for i in mem], step, pos_of[ix[sel]])
+        return out
+    return slack
 
 
 def test_update_step_with_grouped_standardisation(orc, T):
@@ -645,8 +676,10 @@ def test_update_step_with_grouped_standardisation(orc, T):
     orc.update_step(w, offsets, list(range(1, n + 1)), [1] * n, subs, rhat, np.float32(5e-4), np.float32(sig),
                     S.SCALE_ALPHA_OVER_N, index=index)
     _sync(T)
-    assert np.array_equal(to_host(rn), rhat)
-    assert bf16_close(to_host(dw), w)
+    assert zscore_close(to_host(rn), rhat, r, subs)
+    slack = _step_slack(orc, d, offsets, index, list(range(1, n + 1)), [1] * n, subs.tolist(), rhat, 5e-4, sig,
+                        S.SCALE_ALPHA_OVER_N)
+    assert bf16_update_close(to_host(dw), w, slack)
 
 
 @pytest.mark.parametrize("d,chunk,K", [(1000, 8, 3), ((1 << 20) + 5, 64, 8), (10000003, 4096, 16), (65536, 65536, 1)])

@@ -63,3 +63,40 @@ def test_zscore_bound_rejects_plausible_mistakes():
     zero_ref, _ = O.normalize(const, O.NORM_Z)
     assert zscore_close(np.zeros(16, np.float32), zero_ref, const)
     assert not zscore_close(np.full(16, 1e-30, np.float32), zero_ref, const)
+
+
+def _device_order_update(w_bits, seeds, signs, rnorm, step, j0=0):
+    """An update evaluated the way the device does it: fp64 coefficients
+    rounded to fp32, an fp32 multiply-add chain over the streams in order of
+    first appearance (each step rounded once), one fp32 fma with the fp32
+    step, round to bf16."""
+    coef = {}
+    for sd, sg, r in zip(seeds, signs, rnorm):
+        coef[sd] = coef.get(sd, 0.0) + float(sg) * float(r)
+    n = len(w_bits)
+    acc = np.zeros(n, dtype=np.float32)
+    for sd, c in coef.items():
+        z = O.normals(sd, j0, n).astype(np.float64)
+        acc = (np.float64(np.float32(c)) * z + acc.astype(np.float64)).astype(np.float32)
+    w = (w_bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    x = (np.float64(np.float32(step)) * acc.astype(np.float64) + w).astype(np.float32)
+    return S.f32_to_bf16_bits(x)
+
+
+@pytest.mark.parametrize("n,antithetic", [(30, False), (64, True)])
+def test_bf16_update_bound_accepts_fp32_accumulation(n, antithetic):
+    from tests.gpu_helpers import bf16_update_close, update_slack, update_step_size
+
+    seeds = [s for s in range(1, n // 2 + 1) for _ in (0, 1)] if antithetic else list(range(1, n + 1))
+    signs = [1, -1] * (n // 2) if antithetic else [1] * n
+    rnorm, _ = O.normalize(S.rewards("uniform", n, 17), O.NORM_Z)
+    w = S.host_weights(1 << 14, S.BF16, 3)
+    alpha, sigma = np.float32(5e-4), np.float32(2.25e-3)
+    step = update_step_size(alpha, sigma, n, 0)
+    ref = w.copy()
+    O.update(ref, 0, len(w), seeds, signs, rnorm, alpha, sigma, 0)
+    got = _device_order_update(w, seeds, signs, rnorm, step)
+    slack = lambda k: update_slack(O, seeds, signs, rnorm, step, k)
+    assert bf16_update_close(got, ref, slack)
+    wrong = _device_order_update(w, seeds, [-signs[0]] + signs[1:], rnorm, step)     # one member's sign flipped
+    assert not bf16_update_close(wrong, ref, slack)
