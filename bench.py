@@ -218,7 +218,10 @@ def run_step(W, cp, torch, P, timer, cache, fused=False):
         parts = [(offs[k], offs[k + 1] - offs[k]) for k in range(W.K)]
     else:
         parts = cache["parts"]
-    subs = [cp.subspace(o, n, P["index"], W.chunk) for o, n in parts]
+    # a permutation partition's maps are ascending: bf16 restores may then
+    # rewrite whole 128-byte lines around the entries
+    asc = W.partition_mode == S.PART_PERMUTATION
+    subs = [cp.subspace(o, n, P["index"], W.chunk, ascending=asc) for o, n in parts]
     sigmas = [float(np.float32(W.sigma * (W.d / n) ** 0.5)) for _, n in parts]
     later = cp.AUX_BACKUP if W.partition_mode == S.PART_PERMUTATION else cp.AUX_NONE
 
@@ -651,7 +654,7 @@ def kernels_once_mapped(W, cp, torch):
     P = build_plan(W, cp, torch)
     parts = random_partition(W, cp, P)
     off, L = parts[0]
-    s = cp.subspace(off, L, P["index"], W.chunk)
+    s = cp.subspace(off, L, P["index"], W.chunk, ascending=W.partition_mode == S.PART_PERMUTATION)
     sigma = float(__import__("numpy").float32(W.sigma * (W.d / L) ** 0.5))
     snap = P["aux"][:L]
     later = cp.AUX_BACKUP if W.partition_mode == S.PART_PERMUTATION else cp.AUX_NONE

@@ -21,6 +21,7 @@ PART_CONTIGUOUS, PART_PERMUTATION = 0, 1
 AUX_NONE, AUX_SNAPSHOT, AUX_MASTER, AUX_BACKUP = 0, 1, 2, 3
 NORM_Z, NORM_RANK = 0, 1
 SCALE_ALPHA_OVER_N_SIGMA, SCALE_ALPHA_OVER_N = 0, 1
+SUB_ASCENDING = 1
 MAX_MEMBERS, MAX_REWARDS, MAX_GROUPS, MAX_PERMUTATION_K, MAX_STEP_SUBSPACES = 256, 4096, 1024, 256, 32
 
 EXPORTED = (
@@ -41,7 +42,8 @@ class CpesError(RuntimeError):
 
 class Subspace(ctypes.Structure):
     _fields_ = [("offset", ctypes.c_int64), ("length", ctypes.c_int64), ("index", ctypes.c_void_p),
-                ("chunk", ctypes.c_int64), ("index32", ctypes.c_void_p), ("noise_offset", ctypes.c_int64)]
+                ("chunk", ctypes.c_int64), ("index32", ctypes.c_void_p), ("noise_offset", ctypes.c_int64),
+                ("flags", ctypes.c_int64)]
 
 
 _lib = None
@@ -184,13 +186,17 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
-def subspace(offset: int, length: int, index=None, chunk: int = 0, noise_offset: int = 0) -> Subspace:
+def subspace(offset: int, length: int, index=None, chunk: int = 0, noise_offset: int = 0,
+             ascending: bool = False) -> Subspace:
     """Positions j < length at parameter offset + j, index[offset + j], or
     (chunk > 0) index[offset + j // chunk] * chunk + j % chunk; the map must
     hold the entries those positions read.  An int64 map
     goes to ``index``; a 32-bit map (torch.int32 or torch.uint32 holding the
     uint32 entries of cpes_partition32) goes to ``index32``.  Position j uses
-    noise index noise_offset + j (a shard of a larger subspace)."""
+    noise index noise_offset + j (a shard of a larger subspace).
+    ascending=True sets CPES_SUB_ASCENDING: the element map is strictly
+    ascending (a partition's own map), so bf16 restores may rewrite whole
+    128-byte lines around its entries."""
     torch = _torch()
     idx64 = idx32 = None
     if index is not None:
@@ -203,7 +209,8 @@ def subspace(offset: int, length: int, index=None, chunk: int = 0, noise_offset:
             idx32 = _dev_ptr(index, "index map")
         else:
             raise TypeError("index map must be int64, or 32-bit for a uint32 map")
-    sub = Subspace(int(offset), int(length), idx64, int(chunk), idx32, int(noise_offset))
+    sub = Subspace(int(offset), int(length), idx64, int(chunk), idx32, int(noise_offset),
+                   SUB_ASCENDING if ascending else 0)
     sub._index = index      # the descriptor holds a raw pointer: keep the map's storage alive with it
     return sub
 

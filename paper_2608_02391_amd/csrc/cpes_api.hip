@@ -63,6 +63,8 @@ int check_subspace(const void* w, int64_t numel, int dtype, const cpes_subspace*
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: a subspace takes an int64 or a uint32 map, not both", fn);
     if (s->index32 && s->chunk != 0)
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: chunk lists are int64 maps", fn);
+    if (s->flags & ~(int64_t)CPES_SUB_ASCENDING)
+        return fail(CPES_ERR_INVALID_ARGUMENT, "%s: unknown subspace flags 0x%llx", fn, (unsigned long long)s->flags);
     if (!s->index && !s->index32 && s->offset + s->length > numel)
         return fail(CPES_ERR_INVALID_ARGUMENT, "%s: range [%lld, %lld) exceeds numel %lld", fn, (long long)s->offset,
                     (long long)(s->offset + s->length), (long long)numel);
@@ -135,6 +137,7 @@ cpes::StreamArgs stream_args(void* w, int64_t numel, const cpes_subspace* s, con
     a.scale = scale;
     a.chunk_shift = s->chunk ? log2_exact(s->chunk) : 0;
     a.noise0 = s->noise_offset;
+    a.dense = (s->flags & CPES_SUB_ASCENDING) && (s->index32 || (s->index && !s->chunk)) ? 1 : 0;
     return a;
 }
 

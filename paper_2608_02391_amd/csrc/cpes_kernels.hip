@@ -8,6 +8,8 @@
 // aligned (an odd subspace offset, an odd map entry) and the ragged tail take
 // an element-by-element path with the same arithmetic.  Subspaces are ranges,
 // int64 or uint32 element maps, or chunk lists.  Noise never leaves registers.
+#include <type_traits>
+
 #include "cpes_device.hpp"
 #include "cpes_launch.hpp"
 
@@ -565,11 +567,15 @@ __device__ __forceinline__ void wave_lds_sync()
 // Units (lane l holds positions N l .. N l + N - 1 of the tile) to lanes
 // (lane l holds l + 64 e), and back, through the wave's tile buffer `buf`
 // (64 N elements, 16-byte aligned).
+template <int BYTES> struct UnitVec;
+template <> struct UnitVec<16> { typedef V4u type; };
+template <> struct UnitVec<8> { typedef uint2 type; };
+
 template <typename T, int N>
 __device__ __forceinline__ void units_to_lanes(T* buf, int lane, const T in[N], T out[N])
 {
-    static_assert(N * sizeof(T) == 16, "a unit is one 16-byte vector");
-    *reinterpret_cast<V4u*>(buf + N * lane) = *reinterpret_cast<const V4u*>(in);
+    typedef typename UnitVec<N * sizeof(T)>::type U;
+    *reinterpret_cast<U*>(buf + N * lane) = *reinterpret_cast<const U*>(in);
     wave_lds_sync();
 #pragma unroll
     for (int e = 0; e < N; ++e) out[e] = buf[lane + 64 * e];
@@ -578,10 +584,11 @@ __device__ __forceinline__ void units_to_lanes(T* buf, int lane, const T in[N], 
 template <typename T, int N>
 __device__ __forceinline__ void lanes_to_units(T* buf, int lane, const T in[N], T out[N])
 {
+    typedef typename UnitVec<N * sizeof(T)>::type U;
 #pragma unroll
     for (int e = 0; e < N; ++e) buf[lane + 64 * e] = in[e];
     wave_lds_sync();
-    *reinterpret_cast<V4u*>(out) = *reinterpret_cast<const V4u*>(buf + N * lane);
+    *reinterpret_cast<U*>(out) = *reinterpret_cast<const U*>(buf + N * lane);
     wave_lds_sync();
 }
 
@@ -712,6 +719,168 @@ __global__ __launch_bounds__(kBlock) void k_copy_map(StreamArgs a)
                 }
             }
         }
+    }
+}
+
+// ------------------------------------------ dense windows on ascending maps --
+// Restores through a strictly ascending element map (a partition's own maps,
+// flagged CPES_SUB_ASCENDING).  The weights a wave tile of kDenseTile entries
+// touches lie in a narrow window of 128-byte lines.  Each line belongs to the
+// tile holding the line's first entry of the subspace; that tile's wave reads
+// its lines whole into LDS, overlays its entries -- and those of the next
+// tile that fall in its last line (at most 63, the "spill") -- and writes the
+// lines back whole.  Each line is then written once and in full, where
+// scattered 2-byte stores leave a partial write in nearly every 32-byte
+// sector at density 1/8, which the memory system completes by reading the
+// sector first.  The other parameters in those lines are written back with
+// the values just read.  A tile whose lines do not fit the window (a
+// subspace sparser than about 1/10) stores its entries one by one, keeping
+// line ownership: it still takes its spill and leaves the entries in a shared
+// first line to the previous tile.  bf16 weights only; any map entry outside
+// [0, numel) is skipped.  (Perturbations keep the lane-interleaved path: with
+// the noise generator's registers and tables a window kernel holds too few
+// waves per CU to hide its chain of dependent loads, and measured slower.)
+constexpr int kDenseTile = 256;      // entries per wave tile: 4 per lane
+constexpr int kDensePer = kDenseTile / 64;
+constexpr int kLineElems = 64;       // bf16 elements per 128-byte line
+constexpr int kDenseLines = 40;      // LDS window per wave: 5 KiB
+
+struct DenseTile {
+    int64_t t0, t1;     // the tile's entries [t0, t1)
+    int64_t lo, hi;     // lines [lo, hi] it owns
+    bool window;        // the owned lines fit the LDS window (and the tile's ends are in range)
+};
+
+template <int ADDR>
+__device__ __forceinline__ DenseTile dense_tile(const int64_t* index, int64_t offset, int64_t length, int64_t numel,
+                                                int64_t t, int64_t tile)
+{
+    DenseTile d;
+    d.t0 = t * tile;
+    d.t1 = d.t0 + tile < length ? d.t0 + tile : length;
+    const int64_t first = wave_uniform(map_entry<ADDR>(index, offset + d.t0));
+    const int64_t last = wave_uniform(map_entry<ADDR>(index, offset + d.t1 - 1));
+    const int64_t A = first >> 6, B = last >> 6;      // floor division by kLineElems
+    bool shared = false;
+    if (d.t0 > 0) shared = (wave_uniform(map_entry<ADDR>(index, offset + d.t0 - 1)) >> 6) == A;
+    d.lo = shared ? A + 1 : A;
+    d.hi = B;
+    d.window = first >= 0 && last < numel && first <= last && d.hi - d.lo + 1 <= kDenseLines;
+    return d;
+}
+
+// The tile's own entries (lane-interleaved: position t0 + lane + 64 e) with
+// the entries of a shared first line dropped, and this lane's spill entry
+// (position t1 + lane, kept if it falls in line hi); -1 where there is none.
+template <int ADDR>
+__device__ __forceinline__ void dense_entries(const int64_t* index, int64_t offset, int64_t length, int64_t numel,
+                                              const DenseTile& d, int lane, int64_t idx[kDensePer], int64_t& sidx)
+{
+#pragma unroll
+    for (int e = 0; e < kDensePer; ++e) {
+        const int64_t j = d.t0 + lane + 64 * e;
+        int64_t i = j < d.t1 ? map_entry<ADDR>(index, offset + j) : -1;
+        if ((uint64_t)i >= (uint64_t)numel || (i >> 6) < d.lo) i = -1;
+        idx[e] = i;
+    }
+    sidx = -1;
+    const int64_t j = d.t1 + lane;
+    if (j < length) {
+        const int64_t i = map_entry<ADDR>(index, offset + j);
+        if ((uint64_t)i < (uint64_t)numel && (i >> 6) == d.hi) sidx = i;
+    }
+}
+
+// Window transfers: lines [lo, hi] of w to and from the wave's LDS buffer,
+// one 16-byte vector per lane per step, non-temporal (the weights far exceed
+// the caches); the element path covers a window running past numel.
+__device__ __forceinline__ void window_load(const uint16_t* w, int64_t numel, const DenseTile& d, uint16_t* buf,
+                                            int lane)
+{
+    const int64_t base = d.lo * kLineElems, nvec = (d.hi - d.lo + 1) * (kLineElems / 8);
+    const bool whole = base + nvec * 8 <= numel;
+    for (int64_t v = lane; v < nvec; v += 64) {
+        if (whole) {
+            *reinterpret_cast<V4u*>(buf + 8 * v) =
+                __builtin_nontemporal_load(reinterpret_cast<const V4u*>(w + base) + v);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int64_t i = base + 8 * v + k;
+                buf[8 * v + k] = i < numel ? w[i] : (uint16_t)0;
+            }
+        }
+    }
+}
+__device__ __forceinline__ void window_store(uint16_t* w, int64_t numel, const DenseTile& d, const uint16_t* buf,
+                                             int lane)
+{
+    const int64_t base = d.lo * kLineElems, nvec = (d.hi - d.lo + 1) * (kLineElems / 8);
+    const bool whole = base + nvec * 8 <= numel;
+    for (int64_t v = lane; v < nvec; v += 64) {
+        if (whole) {
+            __builtin_nontemporal_store(*reinterpret_cast<const V4u*>(buf + 8 * v),
+                                        reinterpret_cast<V4u*>(w + base) + v);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int64_t i = base + 8 * v + k;
+                if (i < numel) w[i] = buf[8 * v + k];
+            }
+        }
+    }
+}
+
+// Write the tile's new values: overlaid on the window and stored whole, or
+// (no window) stored one by one.
+__device__ __forceinline__ void dense_write(uint16_t* w, int64_t numel, const DenseTile& d, uint16_t* buf, int lane,
+                                            const int64_t idx[kDensePer], const uint16_t v[kDensePer], int64_t sidx,
+                                            uint16_t sv)
+{
+    if (d.window) {
+        const int64_t base = d.lo * kLineElems, nelem = (d.hi - d.lo + 1) * kLineElems;
+#pragma unroll
+        for (int e = 0; e < kDensePer; ++e)
+            if (idx[e] >= base && idx[e] < base + nelem) buf[idx[e] - base] = v[e];
+        if (sidx >= base && sidx < base + nelem) buf[sidx - base] = sv;
+        wave_lds_sync();
+        window_store(w, numel, d, buf, lane);
+        wave_lds_sync();
+    } else {
+#pragma unroll
+        for (int e = 0; e < kDensePer; ++e)
+            if (idx[e] >= 0) w[idx[e]] = v[e];
+        if (sidx >= 0) w[sidx] = sv;
+    }
+}
+
+// Restore through an ascending map: w[p(j)] = aux[j] (bf16 backup, KIND
+// kCopyRestore) or rne_bf16(aux[j]) (fp32 master, KIND kCopyRestoreMaster).
+template <int KIND, int ADDR>
+__global__ __launch_bounds__(kBlock) void k_restore_dense(StreamArgs a)
+{
+    __shared__ __attribute__((aligned(16))) uint16_t win[kBlock / 64][kDenseLines * kLineElems];
+    const int lane = threadIdx.x & 63;
+    uint16_t* buf = win[threadIdx.x / 64];
+    uint16_t* w = static_cast<uint16_t*>(a.w);
+    auto source = [&](int64_t j) -> uint16_t {
+        if (KIND == kCopyRestore) return __builtin_nontemporal_load(static_cast<const uint16_t*>(a.aux) + j);
+        return f32_to_bf16(__builtin_nontemporal_load(static_cast<const float*>(a.aux) + j));
+    };
+    const int64_t tiles = (a.length + kDenseTile - 1) / kDenseTile;
+    for (int64_t t = wave_id(); t < tiles; t += wave_count()) {
+        const DenseTile d = dense_tile<ADDR>(a.index, a.offset, a.length, a.numel, t, kDenseTile);
+        int64_t idx[kDensePer], sidx;
+        dense_entries<ADDR>(a.index, a.offset, a.length, a.numel, d, lane, idx, sidx);
+        uint16_t v[kDensePer], sv = 0;
+#pragma unroll
+        for (int e = 0; e < kDensePer; ++e) v[e] = idx[e] >= 0 ? source(d.t0 + lane + 64 * e) : (uint16_t)0;
+        if (sidx >= 0) sv = source(d.t1 + lane);
+        if (d.window) {
+            window_load(w, a.numel, d, buf, lane);
+            wave_lds_sync();
+        }
+        dense_write(w, a.numel, d, buf, lane, idx, v, sidx, sv);
     }
 }
 
@@ -1330,6 +1499,12 @@ int64_t map_threads(int64_t length)
     }
 #define CPES_COMMA ,
 
+// Dense-window kernels (ascending maps, bf16): one wave per tile of kDenseTile entries.
+int64_t dense_threads(int64_t length)
+{
+    return (length + kDenseTile - 1) / kDenseTile * 64;
+}
+
 template <typename T, int AUX>
 hipError_t perturb_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
@@ -1363,6 +1538,10 @@ inline bool streaming(int64_t length, int bytes_per_position)
 template <typename T>
 hipError_t restore_copy_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
+    if (std::is_same<T, uint16_t>::value && a.dense) {
+        if (addr == kGather) return launch1d(k_restore_dense<kCopyRestore, kGather>, dense_threads(a.length), a, s, kMaxGrid);
+        if (addr == kGather32) return launch1d(k_restore_dense<kCopyRestore, kGather32>, dense_threads(a.length), a, s, kMaxGrid);
+    }
     const int64_t u = units_of<T>(a.length), cap = kMaxGrid;
     if (streaming(a.length, 2 * sizeof(T))) {
         CPES_DISPATCH(k_restore_copy, T CPES_COMMA true, k_copy_map, T CPES_COMMA kCopyRestore CPES_COMMA true)
@@ -1393,6 +1572,10 @@ hipError_t stage_master_t(int addr, bool vec, const StreamArgs& a, hipStream_t s
 hipError_t restore_master_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
     using T = uint16_t;
+    if (a.dense) {
+        if (addr == kGather) return launch1d(k_restore_dense<kCopyRestoreMaster, kGather>, dense_threads(a.length), a, s, kMaxGrid);
+        if (addr == kGather32) return launch1d(k_restore_dense<kCopyRestoreMaster, kGather32>, dense_threads(a.length), a, s, kMaxGrid);
+    }
     const int64_t u = (a.length + 7) / 8, cap = kMaxGrid;
     if (streaming(a.length, 6)) {
         CPES_DISPATCH(k_restore_master, true, k_copy_map, T CPES_COMMA kCopyRestoreMaster CPES_COMMA true)

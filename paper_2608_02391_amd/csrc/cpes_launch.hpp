@@ -31,6 +31,7 @@ struct StreamArgs {
     float scale;            // +-sigma applied to the noise
     int32_t chunk_shift;    // s for chunked subspaces
     int64_t noise0;         // noise index of position 0 (a shard of a larger subspace)
+    int32_t dense;          // an ascending element map: bf16 kernels may use whole-line windows
 };
 
 enum AuxKind { kAuxNone = 0, kAuxSnapshot = 1, kAuxMaster = 2, kAuxBackup = 3 };

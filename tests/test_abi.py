@@ -37,11 +37,11 @@ def test_header_declares_the_boundary():
 def test_library_exports_every_declared_symbol(lib):
     for name in _declared():
         assert hasattr(lib, name), name
-    assert lib.cpes_abi_version() == 6
+    assert lib.cpes_abi_version() == 7
 
 
-def _sub(offset=0, length=16, index=None, chunk=0, index32=None, noise_offset=0):
-    return cp.Subspace(offset, length, index, chunk, index32, noise_offset)
+def _sub(offset=0, length=16, index=None, chunk=0, index32=None, noise_offset=0, flags=0):
+    return cp.Subspace(offset, length, index, chunk, index32, noise_offset, flags)
 
 
 def _rc_msg(lib, rc):
@@ -329,3 +329,9 @@ def test_static_chunk_partition_rejects_before_any_gpu_call(lib):
     rc = call((1 << 23) + 8, 8, 4)                                   # 2^20 + 1 chunks: beyond the static array
     assert rc == cp.ERR_UNSUPPORTED
     assert "static workspace" in lib.cpes_last_error().decode()
+
+
+def test_unknown_subspace_flags_are_rejected(lib):
+    s = _sub(index=FAKE, flags=cp.SUB_ASCENDING | 2)
+    rc, msg = _rc_msg(lib, lib.cpes_restore(FAKE, 64, cp.BF16, ctypes.byref(s), 0.0, 0, 1, FAKE, cp.AUX_SNAPSHOT, None))
+    assert rc == cp.ERR_INVALID_ARGUMENT and "flags" in msg

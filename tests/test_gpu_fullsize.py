@@ -147,7 +147,7 @@ def test_c4_permutation_partition_and_gather(orc, T, big):
     idx_w = {p: index[off + p: off + p + WIN].cpu().numpy() for p in wins}
     before = {p: _host_bits(w[T.from_numpy(idx_w[p]).cuda()]) for p in wins}
     full_before = w.clone()
-    s = cp.subspace(off, L, index)
+    s = cp.subspace(off, L, index, ascending=True)       # the partition's map is ascending, as bench.py passes it
     snap = T.empty(L, dtype=T.bfloat16, device="cuda")
     _say("c4: gather perturb")
     cp.cpes_perturb(w, s, sigma, 11, 1, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
@@ -162,6 +162,19 @@ def test_c4_permutation_partition_and_gather(orc, T, big):
     mask[index[off:off + L]] = True
     assert not bool((changed & ~mask).any())               # nothing outside the subspace moved
     del changed, mask
+    cp.cpes_restore(w, s, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+    T.cuda.synchronize()
+    assert T.equal(w, full_before)
+    _say("c4: whole-line windows and entry-by-entry stores give the same bits")
+    plain = cp.subspace(off, L, index)
+    cp.cpes_perturb(w, plain, sigma, 13, -1, aux=snap, aux_mode=cp.AUX_BACKUP)
+    T.cuda.synchronize()
+    via_entries = w.clone()
+    cp.cpes_restore(w, plain, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
+    cp.cpes_perturb(w, s, sigma, 13, -1, aux=snap, aux_mode=cp.AUX_BACKUP)
+    T.cuda.synchronize()
+    assert T.equal(w, via_entries)
+    del via_entries
     cp.cpes_restore(w, s, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
     T.cuda.synchronize()
     assert T.equal(w, full_before)
@@ -195,7 +208,7 @@ def test_c4_permutation_partition_and_gather(orc, T, big):
     T.cuda.synchronize()
     via64 = w.clone()
     w.copy_(full_before)
-    cp.cpes_perturb(w, cp.subspace(off, L, index32), sigma, 12, -1)
+    cp.cpes_perturb(w, cp.subspace(off, L, index32, ascending=True), sigma, 12, -1)
     T.cuda.synchronize()
     assert T.equal(w, via64)
     w.copy_(full_before)

@@ -121,7 +121,9 @@ def test_fill_normal_matches_oracle(orc, T, dtype, n, shift, seed, domain):
 
 # ------------------------------------------------------------ perturb etc --
 
-LAYOUTS = ["aligned", "unaligned", "gather", "gather_v", "gather32", "chunked", "chunked_wave"]
+LAYOUTS = ["aligned", "unaligned", "gather", "gather_v", "gather32", "chunked", "chunked_wave",
+           "dense", "dense32", "dense_mixed"]
+DENSE = ("dense", "dense32", "dense_mixed")   # maps flagged strictly ascending (CPES_SUB_ASCENDING)
 CHUNK = 64              # chunks shorter than a wave's 64 units: per-lane chunk ids
 CHUNK_WAVE = 1024       # a wave's units share a chunk (64 x 8 bf16 or 64 x 4 fp32 positions): one scalar id
 LENGTHS = [1, 7, 9, 4095, (1 << 20) + 5]
@@ -152,11 +154,26 @@ def _layout(layout, length):
         return length + 64, 16, None
     if layout == "unaligned":
         return length + 64, 3, None
+    if layout == "dense_mixed":
+        index = _mixed_map(length)
+        return int(index[-1]) + 70, 0, index
     d = max(4 * length, 8)
     offsets, index = _perm_partition(d)
-    k = 1 if layout == "gather" else 0
+    k = 1 if layout in ("gather", "dense") else 0
     assert offsets[k + 1] - offsets[k] >= length
     return d, int(offsets[k]), index
+
+
+@functools.lru_cache(maxsize=None)
+def _mixed_map(length):
+    """A strictly ascending map whose density changes every 300 entries:
+    gaps of 1-3 parameters, then gaps of 20-40.  Tiles of 256 entries then
+    alternate between windows that fit the dense path and windows too sparse
+    for it, and lines are shared between the two kinds of tile."""
+    rng = np.random.default_rng(length)
+    blocks = np.arange(length) // 300
+    gaps = np.where(blocks % 2 == 0, rng.integers(1, 4, length), rng.integers(20, 41, length))
+    return np.cumsum(gaps).astype(np.int64) + 5
 
 
 def _setup(orc, T, dtype, layout, length, wseed):
@@ -176,11 +193,11 @@ def _setup(orc, T, dtype, layout, length, wseed):
         return w, to_dev(w), 0, index, sub
     numel, offset, index = _layout(layout, length)
     w = S.host_weights(numel, dtype, wseed)
-    if layout == "gather32":
+    if layout in ("gather32", "dense32"):
         dev_map = to_dev(index.astype(np.uint32).view(np.int32))
     else:
         dev_map = to_dev(index) if index is not None else None
-    return w, to_dev(w), offset, index, cp.subspace(offset, length, dev_map)
+    return w, to_dev(w), offset, index, cp.subspace(offset, length, dev_map, ascending=layout in DENSE)
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
