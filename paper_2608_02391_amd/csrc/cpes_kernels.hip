@@ -1402,25 +1402,31 @@ __global__ void k_zero_u32(uint32_t* p)
 }
 
 // RNG-only probe: each thread takes units of 8 positions and, like the update,
-// generates the noise of kRngProbeStreams consecutive seeds for each unit,
-// folding the bits into one word; no memory traffic but one atomic per wave.
+// generates the noise of kRngProbeStreams consecutive seeds for each unit into
+// 8 independent fp32 accumulators; the accumulators' bits are folded into one
+// word at the end.  No memory traffic but one atomic per wave.
 constexpr int kRngProbeStreams = 16;
 
 __global__ __launch_bounds__(kBlock) void k_rng_probe(uint64_t seed, int64_t units, uint32_t* sink)
 {
     const BmTables* tb = stage_bm_tables<kBlock>();
-    uint32_t acc = 0;
+    float acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
     for (int64_t u = global_tid(); u < units; u += grid_stride()) {
         for (int st = 0; st < kRngProbeStreams; ++st) {
             const uint64_t key = seed + (uint64_t)st;
             float z[8];
             normals8((uint32_t)key, (uint32_t)(key >> 32), (uint64_t)u * 2u, tb, z);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc ^= __float_as_uint(z[e]);
+            for (int e = 0; e < 8; ++e) acc[e] = __builtin_fmaf(0.5f, z[e], acc[e]);
         }
     }
-    for (int off = 32; off > 0; off >>= 1) acc ^= __shfl_xor(acc, off);
-    if ((threadIdx.x & 63) == 0) atomicXor(sink, acc);
+    uint32_t x = 0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x ^= __float_as_uint(acc[e]);
+    for (int off = 32; off > 0; off >>= 1) x ^= __shfl_xor(x, off);
+    if ((threadIdx.x & 63) == 0) atomicXor(sink, x);
 }
 
 // Measurement references with nothing but the memory traffic.  The plainest
