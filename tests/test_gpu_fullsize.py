@@ -228,7 +228,7 @@ def test_c5_master_iteration(orc, T, big):
     full_before = w.clone()
     s = cp.subspace(off, L)
     master = T.empty(L, dtype=T.float32, device="cuda")
-    _say("c5: stage master and bf16 backup, perturb from master, restore from the backup and from master")
+    _say("c5: stage master and bf16 backup; perturb from the backup (as bench.py) and from the master; restore")
     cp.cpes_stage_master(w, s, master)
     backup = T.empty(L, dtype=T.bfloat16, device="cuda")
     cp.cpes_backup(w, s, backup)                       # the schedule bench.py times
@@ -237,7 +237,15 @@ def test_c5_master_iteration(orc, T, big):
     assert T.equal(backup, full_before[off:off + L])
     seeds = W.member_seeds(t)
     for m in (0, 1, 127):
-        cp.cpes_perturb(w, s, sigma, seeds[m], W.signs[m], aux=master, aux_mode=cp.AUX_MASTER)
+        # members perturb from the bf16 backup, the schedule bench.py times; member 1 also
+        # from the master, which must give the same 4 G weights bit for bit
+        cp.cpes_perturb(w, s, sigma, seeds[m], W.signs[m], aux=backup, aux_mode=cp.AUX_BACKUP)
+        if m == 1:
+            via_backup = w.clone()
+            cp.cpes_perturb(w, s, sigma, seeds[m], W.signs[m], aux=master, aux_mode=cp.AUX_MASTER)
+            T.cuda.synchronize()
+            assert T.equal(w, via_backup)
+            del via_backup
         T.cuda.synchronize()
         p = wins[m % len(wins)]
         ref = before[p].copy()

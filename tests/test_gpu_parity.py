@@ -302,9 +302,12 @@ def test_device_backup_is_the_oracle_snapshot(orc, T, dtype, layout, length):
 
 @pytest.mark.parametrize("layout", ["aligned", "gather", "chunked"])
 def test_master_loop_restores_from_a_bf16_backup(orc, T, layout):
-    """With an fp32 master staged from w, restoring each member from a bf16
-    backup of w gives the same bits as restoring from the master (w is the
-    master rounded to bf16 when both are taken), also after an update."""
+    """With an fp32 master staged from w, a bf16 backup of w taken at the
+    same time holds the master's values exactly (w is the master rounded to
+    bf16, the master f32 of w).  So perturbing each member from the backup
+    and restoring from it -- the schedule bench.py times for c5 -- gives the
+    same bits as perturbing from and restoring from the master, member by
+    member and after the update."""
     length = 200003
     w, dw, off, index, s = _setup(orc, T, S.BF16, layout, length, 91)
     dw2 = dw.clone()
@@ -319,7 +322,7 @@ def test_master_loop_restores_from_a_bf16_backup(orc, T, layout):
         cp.cpes_backup(dw2, s, b)
         for seed, sign in members:
             cp.cpes_perturb(dw, s, 2e-3, seed + it, sign, aux=master, aux_mode=cp.AUX_MASTER)
-            cp.cpes_perturb(dw2, s, 2e-3, seed + it, sign, aux=master2, aux_mode=cp.AUX_MASTER)
+            cp.cpes_perturb(dw2, s, 2e-3, seed + it, sign, aux=b, aux_mode=cp.AUX_BACKUP)
             _sync(T)
             assert T.equal(dw.view(T.int16), dw2.view(T.int16))
             cp.cpes_restore(dw, s, aux=master, aux_mode=cp.AUX_MASTER)
