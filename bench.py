@@ -49,10 +49,10 @@ KERNEL_SOURCES = ("cpes_kernels.hip", "cpes_device.hpp", "cpes_bm_tables.hpp", "
 # hold for the kernel sources whose SHA-256 is `sources_sha256`; with other
 # sources they are reported as stale and not used.
 MEASURED = {
-    "sources_sha256": "cbaf4b62df76913705e8400b942fc9bc836f1dcaf4ef7d0a6f8b20a03c47b434",
-    "perturb": {"valu_per_normal": 33.82, "hbm_bytes_first": 6.0, "hbm_bytes_rest": 4.0, "clock_ghz": 2.32},
+    "sources_sha256": "1c2d83d8f21dc94cad67b3a1082a1b337a9e6e1490cef5a72f1d586983b09562",
+    "perturb": {"valu_per_normal": 33.82, "hbm_bytes_first": 6.0, "hbm_bytes_rest": 4.0, "clock_ghz": 2.30},
     "perturb_master": {"valu_per_normal": 34.07, "hbm_bytes": 4.0, "clock_ghz": 2.39},
-    "update": {"valu_per_normal": 31.29, "hbm_bytes": 4.0, "clock_ghz": 2.32},
+    "update": {"valu_per_normal": 31.29, "hbm_bytes": 4.0, "clock_ghz": 2.33},
     "update_master": {"valu_per_normal": 31.20, "hbm_bytes": 10.0, "clock_ghz": 2.34},
     "restore": {"hbm_bytes": 4.0},
 }
@@ -218,8 +218,8 @@ def run_step(W, cp, torch, P, timer, cache, fused=False):
         parts = [(offs[k], offs[k + 1] - offs[k]) for k in range(W.K)]
     else:
         parts = cache["parts"]
-    # a permutation partition's maps are ascending: bf16 restores may then
-    # rewrite whole 128-byte lines around the entries
+    # a permutation partition's maps are ascending: bf16 perturbations and
+    # restores may then rewrite whole 128-byte lines around the entries
     asc = W.partition_mode == S.PART_PERMUTATION
     subs = [cp.subspace(o, n, P["index"], W.chunk, ascending=asc) for o, n in parts]
     sigmas = [float(np.float32(W.sigma * (W.d / n) ** 0.5)) for _, n in parts]
@@ -647,8 +647,10 @@ def kernels_once_mapped(W, cp, torch):
     """The same for a partitioned workload (c4, c4u, c4c): partition once, then
     one warm-up and one measured launch of each kernel of subspace 0 (perturb
     taking the backup, perturb from the backup or in place, restore, update,
-    and for element maps the plain gather and scatter probes), plus torch's
-    copy of the subspace's bf16 bytes as the plain-copy reference."""
+    and for element maps the plain gather and scatter probes and, through the
+    map left unflagged, the entry-by-entry perturbation from the backup and
+    restore), plus torch's copy of the subspace's bf16 bytes as the plain-copy
+    reference."""
     import synthetic as S
 
     P = build_plan(W, cp, torch)
@@ -670,6 +672,9 @@ def kernels_once_mapped(W, cp, torch):
         if W.partition_mode == S.PART_PERMUTATION:
             cp.cpes_probe_map_copy(P["w"], s, dst, 0)
             cp.cpes_probe_map_copy(P["w"], s, dst, 1)
+            entries = cp.subspace(off, L, P["index"], W.chunk)
+            cp.cpes_perturb(P["w"], entries, sigma, 4, -1, aux=snap, aux_mode=cp.AUX_BACKUP)
+            cp.cpes_restore(P["w"], entries, aux=snap, aux_mode=cp.AUX_SNAPSHOT)
         dst.copy_(P["w"][:L])
     torch.cuda.synchronize()
     print(json.dumps({"kernels_once": f"{W.name} subspace 0", "positions": L}), flush=True)

@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define CPES_ABI_VERSION 7
+#define CPES_ABI_VERSION 8
 
 /* Exported symbols (the library is built with hidden default visibility). */
 #define CPES_API __attribute__((visibility("default")))
@@ -107,15 +107,16 @@ typedef struct cpes_subspace {
 /* cpes_subspace.flags.  CPES_SUB_ASCENDING: the element map (index or
  * index32) is strictly ascending over the subspace's positions, as the maps
  * of cpes_partition and cpes_partition32 are.  With bf16 weights the
- * restores (cpes_restore from a backup or a master, cpes_restore_from_host)
- * may then read and write whole 128-byte lines of the weights around the
- * subspace's entries (once each), writing the other parameters of those
- * lines back with the values just read, instead of storing the entries one
- * by one: on a dense subspace every line is then written in full rather than
- * partially.  Results are those of the entry-by-entry path, provided nothing
- * else writes the same weights while the call runs; with a map that is not
- * strictly ascending they are undefined (every access stays within w and the
- * map).  Ignored for other calls, contiguous and chunked subspaces and fp32
+ * perturbations (cpes_perturb, every aux mode) and the restores (cpes_restore
+ * from a backup or a master, cpes_restore_from_host) may then read and write
+ * whole 128-byte lines of the weights around the subspace's entries (once
+ * each), writing the other parameters of those lines back with the values
+ * just read, instead of storing the entries one by one: on a dense subspace
+ * almost every line is then written in full rather than partially.  Results
+ * are those of the entry-by-entry path, provided nothing else writes the same
+ * weights while the call runs; with a map that is not strictly ascending they
+ * are undefined (every access stays within w, the map and the side buffer).
+ * Ignored for other calls, contiguous and chunked subspaces and fp32
  * weights. */
 #define CPES_SUB_ASCENDING 1
 

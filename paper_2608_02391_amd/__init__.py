@@ -195,8 +195,8 @@ def subspace(offset: int, length: int, index=None, chunk: int = 0, noise_offset:
     uint32 entries of cpes_partition32) goes to ``index32``.  Position j uses
     noise index noise_offset + j (a shard of a larger subspace).
     ascending=True sets CPES_SUB_ASCENDING: the element map is strictly
-    ascending (a partition's own map), so bf16 restores may rewrite whole
-    128-byte lines around its entries."""
+    ascending (a partition's own map), so bf16 perturbations and restores may
+    rewrite whole 128-byte lines around its entries."""
     torch = _torch()
     idx64 = idx32 = None
     if index is not None:

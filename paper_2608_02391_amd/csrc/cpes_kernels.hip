@@ -8,6 +8,7 @@
 // aligned (an odd subspace offset, an odd map entry) and the ragged tail take
 // an element-by-element path with the same arithmetic.  Subspaces are ranges,
 // int64 or uint32 element maps, or chunk lists.  Noise never leaves registers.
+#include <algorithm>
 #include <type_traits>
 
 #include "cpes_device.hpp"
@@ -737,9 +738,8 @@ __global__ __launch_bounds__(kBlock) void k_copy_map(StreamArgs a)
 // subspace sparser than about 1/10) stores its entries one by one, keeping
 // line ownership: it still takes its spill and leaves the entries in a shared
 // first line to the previous tile.  bf16 weights only; any map entry outside
-// [0, numel) is skipped.  (Perturbations keep the lane-interleaved path: with
-// the noise generator's registers and tables a window kernel holds too few
-// waves per CU to hide its chain of dependent loads, and measured slower.)
+// [0, numel) is skipped.  (Perturbations tile without a spill, below: the
+// spill's entries would need the noise of the next tile's positions.)
 constexpr int kDenseTile = 256;      // entries per wave tile: 4 per lane
 constexpr int kDensePer = kDenseTile / 64;
 constexpr int kLineElems = 64;       // bf16 elements per 128-byte line
@@ -881,6 +881,168 @@ __global__ __launch_bounds__(kBlock) void k_restore_dense(StreamArgs a)
             wave_lds_sync();
         }
         dense_write(w, a.numel, d, buf, lane, idx, v, sidx, sv);
+    }
+}
+
+// ----------------------------------- whole-line perturbations (ascending) --
+// A perturbation through an ascending map writes whole lines too, on fixed
+// tiles of kDenseTile entries but without a spill: the lines strictly inside
+// a tile's span hold no entry of another tile and go through the tile's LDS
+// window; its entries in a first or last line shared with a neighbouring tile
+// are stored one by one, as the neighbour stores its own entries there, so a
+// line written whole has no other writer.  Lane l takes the tile's positions
+// t0 + 4 l .. t0 + 4 l + 3, which are one Philox block of noise, and moves
+// the map and the side buffers as 8- or 16-byte vectors where aligned.  The
+// perturbation is that of Eq. (8) on a subspace of the partition of Eq. (7).
+// (Restores tiled this way, with no noise to generate, measured a few per
+// cent slower than the spill kernel above, which they therefore keep.)
+template <int ADDR>
+__device__ __forceinline__ DenseTile edge_tile(const int64_t* index, int64_t offset, int64_t length, int64_t numel,
+                                               int64_t t)
+{
+    DenseTile d;
+    d.t0 = t * kDenseTile;
+    d.t1 = d.t0 + kDenseTile < length ? d.t0 + kDenseTile : length;
+    const int64_t first = wave_uniform(map_entry<ADDR>(index, offset + d.t0));
+    const int64_t last = wave_uniform(map_entry<ADDR>(index, offset + d.t1 - 1));
+    const int64_t A = first >> 6, B = last >> 6;
+    const bool prev = d.t0 > 0 && (wave_uniform(map_entry<ADDR>(index, offset + d.t0 - 1)) >> 6) == A;
+    const bool next = d.t1 < length && (wave_uniform(map_entry<ADDR>(index, offset + d.t1)) >> 6) == B;
+    d.lo = prev ? A + 1 : A;
+    d.hi = next ? B - 1 : B;
+    if (d.hi < d.lo) d.hi = d.lo - 1;   // every entry lies in a shared line: an empty window
+    d.window = first >= 0 && last < numel && first <= last && d.hi - d.lo + 1 <= kDenseLines;
+    return d;
+}
+
+// Entries p .. p + 3 of the map (n of them exist; -1 for the others and for
+// entries outside [0, numel)); vector loads when `vec` (16-byte aligned).
+template <int ADDR>
+__device__ __forceinline__ void map_entries4(const int64_t* index, int64_t p, int64_t n, bool vec, int64_t numel,
+                                             int64_t idx[4])
+{
+    if (vec && n >= 4) {
+        if (ADDR == kGather) {
+            const V4u x = *reinterpret_cast<const V4u*>(index + p);
+            const V4u y = *reinterpret_cast<const V4u*>(index + p + 2);
+            idx[0] = (int64_t)(((uint64_t)x[1] << 32) | x[0]);
+            idx[1] = (int64_t)(((uint64_t)x[3] << 32) | x[2]);
+            idx[2] = (int64_t)(((uint64_t)y[1] << 32) | y[0]);
+            idx[3] = (int64_t)(((uint64_t)y[3] << 32) | y[2]);
+        } else {
+            const V4u x = *reinterpret_cast<const V4u*>(reinterpret_cast<const uint32_t*>(index) + p);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) idx[e] = (int64_t)x[e];
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) idx[e] = e < n ? map_entry<ADDR>(index, p + e) : -1;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        if ((uint64_t)idx[e] >= (uint64_t)numel) idx[e] = -1;
+}
+
+// The tile's new values: those in the window (in[e]) overlaid on it and its
+// lines stored whole, the others (in a shared line, or all of them when the
+// tile has no window) stored one by one.
+__device__ __forceinline__ void edge_write(uint16_t* w, int64_t numel, const DenseTile& d, uint16_t* buf, int lane,
+                                           const int64_t idx[4], const bool in[4], int64_t base, const uint16_t v[4])
+{
+    if (d.window) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (in[e]) buf[idx[e] - base] = v[e];
+        wave_lds_sync();
+        window_store(w, numel, d, buf, lane);
+        wave_lds_sync();
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        if (!in[e] && idx[e] >= 0) w[idx[e]] = v[e];
+}
+
+// Workgroups of kDenseBlock threads share one copy of the noise tables; with
+// at most 80 VGPRs, three of them (52 KiB of LDS each) give 6 waves per SIMD,
+// where 256-thread workgroups (32 KiB each) give 5.  Measured on 0.5 G-entry
+// maps: 6-20 % faster, except the perturbation from the backup through an
+// int64 map (3 % slower).
+constexpr int kDenseBlock = 512;
+
+template <int AUX, int ADDR>
+__global__ __launch_bounds__(kDenseBlock, 6) void k_perturb_dense(StreamArgs a)
+{
+    const BmTables* tb = stage_bm_tables<kDenseBlock>();
+    __shared__ __attribute__((aligned(16))) uint16_t win[kDenseBlock / 64][kDenseLines * kLineElems];
+    const int lane = threadIdx.x & 63;
+    uint16_t* buf = win[threadIdx.x / 64];
+    uint16_t* w = static_cast<uint16_t*>(a.w);
+    constexpr uint64_t kEntry = ADDR == kGather ? 8 : 4;
+    const bool vmap = (((uintptr_t)a.index + (uint64_t)a.offset * kEntry) & 15) == 0;
+    const bool vaux = ((uintptr_t)a.aux & (AUX == kAuxMaster ? 15 : 7)) == 0;
+    const int64_t tiles = (a.length + kDenseTile - 1) / kDenseTile;
+    const int64_t waves = (int64_t)gridDim.x * (kDenseBlock / 64);
+    for (int64_t t = (int64_t)blockIdx.x * (kDenseBlock / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x / 64); t < tiles;
+         t += waves) {
+        const DenseTile d = edge_tile<ADDR>(a.index, a.offset, a.length, a.numel, t);
+        const int64_t j0 = d.t0 + 4 * lane;
+        const bool whole = j0 + 4 <= a.length;
+        int64_t idx[4];
+        map_entries4<ADDR>(a.index, a.offset + j0, a.length - j0, vmap, a.numel, idx);
+        float src[4];
+        if (AUX == kAuxBackup) {
+            const uint16_t* b = static_cast<const uint16_t*>(a.aux) + j0;
+            uint16_t o[4];
+            if (vaux && whole) {
+                *reinterpret_cast<uint2*>(o) = *reinterpret_cast<const uint2*>(b);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[e] = j0 + e < a.length ? b[e] : (uint16_t)0;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) src[e] = bf16_to_f32(o[e]);
+        } else if (AUX == kAuxMaster) {
+            const float* m = static_cast<const float*>(a.aux) + j0;
+            if (vaux && whole) {
+                load_f32s<4>(m, src);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) src[e] = j0 + e < a.length ? m[e] : 0.0f;
+            }
+        }
+        float z[4];
+        normals4(a.k0, a.k1, (uint64_t)(a.noise0 + j0) >> 2, tb, z);
+        int64_t base = 0, nelem = 0;
+        if (d.window) {
+            base = d.lo * kLineElems;
+            nelem = (d.hi - d.lo + 1) * kLineElems;
+            window_load(w, a.numel, d, buf, lane);
+            wave_lds_sync();
+        }
+        bool in[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) in[e] = idx[e] >= base && idx[e] < base + nelem;
+        if (AUX == kAuxNone || AUX == kAuxSnapshot) {
+            uint16_t o[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = in[e] ? buf[idx[e] - base] : idx[e] >= 0 ? w[idx[e]] : (uint16_t)0;
+            if (AUX == kAuxSnapshot) {
+                uint16_t* snap = static_cast<uint16_t*>(a.aux) + j0;
+                if (vaux && whole) {
+                    *reinterpret_cast<uint2*>(snap) = *reinterpret_cast<const uint2*>(o);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (j0 + e < a.length) snap[e] = o[e];
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) src[e] = bf16_to_f32(o[e]);
+        }
+        uint16_t v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = f32_to_bf16(__builtin_fmaf(a.scale, z[e], src[e]));
+        edge_write(w, a.numel, d, buf, lane, idx, in, base, v);
     }
 }
 
@@ -1514,6 +1676,13 @@ int64_t dense_threads(int64_t length)
 template <typename T, int AUX>
 hipError_t perturb_t(int addr, bool vec, const StreamArgs& a, hipStream_t s)
 {
+    if (std::is_same<T, uint16_t>::value && a.dense) {
+        const dim3 grid((unsigned)std::min<int64_t>(std::max<int64_t>((dense_threads(a.length) + kDenseBlock - 1) / kDenseBlock, 1),
+                                                    kRngMaxGrid / 2));
+        if (addr == kGather) hipLaunchKernelGGL((k_perturb_dense<AUX, kGather>), grid, dim3(kDenseBlock), 0, s, a);
+        else if (addr == kGather32) hipLaunchKernelGGL((k_perturb_dense<AUX, kGather32>), grid, dim3(kDenseBlock), 0, s, a);
+        if (addr == kGather || addr == kGather32) return hipGetLastError();
+    }
     const int64_t u = units_of<T>(a.length), cap = kRngMaxGrid;
     if (vec) {
         CPES_DISPATCH(k_perturb, T CPES_COMMA AUX, k_perturb_map, T CPES_COMMA AUX CPES_COMMA true)

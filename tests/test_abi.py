@@ -37,7 +37,7 @@ def test_header_declares_the_boundary():
 def test_library_exports_every_declared_symbol(lib):
     for name in _declared():
         assert hasattr(lib, name), name
-    assert lib.cpes_abi_version() == 7
+    assert lib.cpes_abi_version() == 8
 
 
 def _sub(offset=0, length=16, index=None, chunk=0, index32=None, noise_offset=0, flags=0):

@@ -122,8 +122,8 @@ def test_fill_normal_matches_oracle(orc, T, dtype, n, shift, seed, domain):
 # ------------------------------------------------------------ perturb etc --
 
 LAYOUTS = ["aligned", "unaligned", "gather", "gather_v", "gather32", "chunked", "chunked_wave",
-           "dense", "dense32", "dense_mixed"]
-DENSE = ("dense", "dense32", "dense_mixed")   # maps flagged strictly ascending (CPES_SUB_ASCENDING)
+           "dense", "dense_v", "dense32", "dense_mixed"]
+DENSE = ("dense", "dense_v", "dense32", "dense_mixed")   # maps flagged strictly ascending (CPES_SUB_ASCENDING)
 CHUNK = 64              # chunks shorter than a wave's 64 units: per-lane chunk ids
 CHUNK_WAVE = 1024       # a wave's units share a chunk (64 x 8 bf16 or 64 x 4 fp32 positions): one scalar id
 LENGTHS = [1, 7, 9, 4095, (1 << 20) + 5]
@@ -149,7 +149,9 @@ def _layout(layout, length):
     4-way permutation partition of 4 * length indices: subspace 1 ("gather",
     its map starts at an odd entry, so units take the element path) or
     subspace 0 ("gather_v", "gather32": 16-byte map vectors; gather32 passes
-    the map as uint32)."""
+    the map as uint32).  The "dense" layouts are the same maps flagged
+    ascending ("dense_v" at the 16-byte aligned subspace 0), and "dense_mixed"
+    one whose density alternates."""
     if layout == "aligned":
         return length + 64, 16, None
     if layout == "unaligned":
@@ -234,6 +236,35 @@ def test_perturb_matches_oracle(orc, T, dtype, aux, layout, length):
         assert ulp_f32(got[touched], w[touched]).max() <= 1
     if aux == 1:
         assert np.array_equal(to_host(snap_d), snap_h)              # the backup is exact
+
+
+@pytest.mark.parametrize("layout", DENSE)
+@pytest.mark.parametrize("aux", [1, 2, 3])
+@pytest.mark.parametrize("length", [4095, 70001])
+def test_perturb_side_buffer_at_odd_offset(orc, T, aux, layout, length):
+    """A snapshot, master or backup that starts one element past an aligned
+    address (a view into a larger buffer): the side buffer moves element by
+    element and the results are those of the oracle."""
+    w, dw, off, index, s = _setup(orc, T, S.BF16, layout, length, 2000 + length)
+    sigma, seed = np.float32(2.8284e-3), 23 + length
+    w0 = w.copy()
+    if aux == 1:
+        side_h = np.zeros(length, dtype=w.dtype)
+    else:
+        side_h = S.host_weights(length, S.F32 if aux == 2 else S.BF16, 11 + length)
+    big = to_dev(np.concatenate([side_h[:1], side_h]))
+    side_d = big[1:]
+    assert side_d.data_ptr() % 8 != 0
+    cp.cpes_perturb(dw, s, float(sigma), seed, 1, aux=side_d, aux_mode=aux)
+    orc.perturb(w, off, length, sigma, seed, 1, index=index, aux=side_h, aux_mode=aux)
+    _sync(T)
+    got = to_host(dw)
+    touched = np.zeros(w.size, dtype=bool)
+    touched[index[off:off + length]] = True
+    assert np.array_equal(got[~touched], w0[~touched])
+    assert ulp_bf16(got[touched], w[touched]).max() <= 1
+    if aux == 1:
+        assert np.array_equal(to_host(side_d), side_h)
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
