@@ -231,7 +231,9 @@ CPES_API size_t cpes_partition_chunks_workspace_bytes(int64_t d, int64_t chunk, 
  *                               and then perturbing, in one pass.  Every member
  *                               of a step perturbs the same pre-update weights,
  *                               so one backup serves all of them.
- * Parameters outside the subspace are not touched.
+ * Parameters outside the subspace keep their values (through a map flagged
+ * CPES_SUB_ASCENDING, bf16 lines around the entries are rewritten with the
+ * values just read; see cpes_subspace.flags).
  * Errors: w NULL, s NULL, length < 0, contiguous range beyond numel, dtype /
  *   aux_mode unknown, aux NULL when needed, sign not +-1, sigma negative or
  *   not finite, MASTER with fp32 weights -> CPES_ERR_INVALID_ARGUMENT.
