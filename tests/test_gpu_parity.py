@@ -99,6 +99,13 @@ def test_gpu_normal_statistics(T):
     assert abs(z.var(unbiased=False).item() - 1.0) < 5 * np.sqrt(2.0) * se
     assert abs(((z - z.mean()) ** 3).mean().item()) < 5 * np.sqrt(15.0) * se
     assert abs(((z - z.mean()) ** 4).mean().item() - 3.0) < 5 * np.sqrt(96.0) * se
+    # Kolmogorov-Smirnov against the standard normal CDF over all 2^26 values:
+    # the statistic stays below the 0.1 % critical value 1.95 / sqrt(n)
+    zs = T.sort(out).values.double()
+    cdf = T.special.ndtr(zs)
+    upper = T.arange(1, n + 1, dtype=T.float64, device="cuda") / n
+    ks = max((upper - cdf).max().item(), (cdf - (upper - 1.0 / n)).max().item())
+    assert ks < 1.95 / np.sqrt(n), ks
 
 
 @pytest.mark.parametrize("dtype", [S.BF16, S.F32])
@@ -569,13 +576,16 @@ def test_update_mirrored_equal_rewards_is_identity(T):
 def test_degenerate_calls_leave_weights_untouched(T, dtype):
     """sigma = 0 perturbs to the same bits (one fp32 FMA with a zero product,
     then the exact bf16 rounding of an exact value), an empty subspace and a
-    zero step do nothing."""
+    zero step do nothing, and neither do mirrored pairs with equal rewards
+    (each stream's folded coefficient is exactly zero)."""
     w = S.host_weights(70001, dtype, 12)
     dw = to_dev(w)
     s = cp.subspace(1, 70000)
     cp.cpes_perturb(dw, s, 0.0, 3, 1)
     cp.cpes_perturb(dw, cp.subspace(9, 0), 1e-2, 3, 1)
     cp.cpes_update(dw, s, [1, 2], [1, 1], to_dev(np.array([0.3, -0.3], np.float32)), 0.0, 1e-3)
+    cp.cpes_update(dw, s, [5, 5, 6, 6], [1, -1, 1, -1], to_dev(np.array([0.7, 0.7, -0.2, -0.2], np.float32)),
+                   5e-4, 1e-3)
     cp.cpes_restore(dw, cp.subspace(70001, 0), aux=None, aux_mode=cp.AUX_NONE, sigma=1e-3)
     _sync(T)
     assert np.array_equal(to_host(dw), w)
