@@ -738,8 +738,8 @@ __global__ __launch_bounds__(kBlock) void k_copy_map(StreamArgs a)
 // subspace sparser than about 1/10) stores its entries one by one, keeping
 // line ownership: it still takes its spill and leaves the entries in a shared
 // first line to the previous tile.  bf16 weights only; any map entry outside
-// [0, numel) is skipped.  (Perturbations tile without a spill, below: the
-// spill's entries would need the noise of the next tile's positions.)
+// [0, numel) is skipped.  (Perturbations tile without a spill, below, so
+// that a wave generates the noise of its own tile's positions only.)
 constexpr int kDenseTile = 256;      // entries per wave tile: 4 per lane
 constexpr int kDensePer = kDenseTile / 64;
 constexpr int kLineElems = 64;       // bf16 elements per 128-byte line
