@@ -405,7 +405,7 @@ def test_host_backup_round_trip(orc, T, dtype, layout, length):
     assert np.array_equal(to_host(dw), w0)
 
 
-@pytest.mark.parametrize("layout", ["unaligned", "chunked"])
+@pytest.mark.parametrize("layout", ["unaligned", "chunked", "dense_v"])
 def test_host_backup_member_loop(orc, T, layout):
     """One host backup per step, then perturb / restore for every member: each
     member is perturbed from the same pre-update weights (the oracle perturbs
